@@ -1,0 +1,430 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+None of these retypes the oracle's step: each check is a closed form, a
+special case that collapses to a textbook recursion, an identity between
+two separately written oracle functions that the paper proves, an
+invariant, or a number printed in the paper (fixtures in tests/golden/).
+A plausible mistake in the step -- a dropped term, a wrong sign, rows and
+columns swapped, the wrong momentum driving the factors or the drift --
+fails at least one of them (see the note on each test).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+# ----------------------------------------------------------------- bf16
+
+def _all_positive_bf16():
+    bits = np.arange(0x0001, 0x7F80, dtype=np.uint32)       # finite, > 0
+    return (bits << 16).view(np.float32).astype(np.float64)
+
+
+def test_bf16_representable_values_are_fixed_points():
+    v = _all_positive_bf16()
+    assert np.array_equal(O.round_bf16(v), v)
+    assert np.array_equal(O.round_bf16(-v), -v)
+
+
+def test_bf16_midpoints_tie_to_even_and_neighbours_round_to_nearest():
+    v = _all_positive_bf16()
+    lo, hi = v[:-1], v[1:]
+    mid = 0.5 * (lo + hi)                                   # exact in fp64
+    even = np.where(((lo.astype(np.float32).view(np.uint32) >> 16) & 1) == 0, lo, hi)
+    assert np.array_equal(O.round_bf16(mid), even)
+    below = np.nextafter(mid, 0.0)
+    above = np.nextafter(mid, np.inf)
+    assert np.array_equal(O.round_bf16(below), lo)
+    assert np.array_equal(O.round_bf16(above), hi)
+
+
+def test_bf16_agrees_with_torch_on_fp32_inputs():
+    """torch rounds fp32 -> bf16 to nearest-even; on doubles that are exact
+    fp32 values a single rounding from fp64 must give the same result."""
+    rng = _rng(1)
+    f = np.concatenate([
+        rng.standard_normal(200000).astype(np.float32) * np.float32(0.02),
+        (rng.standard_normal(100000) * 1e-38).astype(np.float32),    # subnormal range
+        (rng.standard_normal(100000) * 3e38).astype(np.float32),     # overflow edge
+    ])
+    f = f[np.isfinite(f)]
+    ref = torch.from_numpy(f).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.round_bf16(f.astype(np.float64)), ref)
+
+
+def test_bf16_overflow_and_specials():
+    big = (2.0 - 2.0 ** -7) * 2.0 ** 127
+    assert O.round_bf16(np.array([big]))[0] == big
+    assert np.isinf(O.round_bf16(np.array([(2.0 - 2.0 ** -8) * 2.0 ** 127]))[0])
+    out = O.round_bf16(np.array([0.0, -0.0, np.inf, -np.inf, np.nan]))
+    assert out[0] == 0.0 and out[2] == np.inf and out[3] == -np.inf and np.isnan(out[4])
+
+
+# ---------------------------------------------------------- coefficients
+
+@pytest.mark.parametrize("alpha,h,mu", [(0.1, 1e-3, 1.0), (0.0579, 0.0918, 1.3637e-6),
+                                        (2.8475, 0.4842, 1.9407e-6), (1.0, 0.02, 1.0)])
+def test_coefficients_match_series(alpha, h, mu):
+    """App. A Table, factor update: a = e^{-alpha h}, kappa = (1-a)/(mu alpha).
+    Checked against the Taylor series of (1 - e^{-z})/z, a different route."""
+    a, kappa, d = O.coefficients(O.HParams(h=h, gamma=0.0, alpha=alpha, mu=mu))
+    z = alpha * h
+    series = sum((-z) ** k / math.factorial(k + 1) for k in range(30))
+    assert a == pytest.approx(math.exp(-z), rel=1e-15)
+    assert kappa == pytest.approx(h / mu * series, rel=1e-13)
+    assert d == 1.0
+
+
+def test_coefficients_alpha_zero_limit_and_damping():
+    a, kappa, d = O.coefficients(O.HParams(h=0.5, gamma=0.3, alpha=0.0, mu=4.0))
+    assert a == 1.0 and kappa == 0.125 and d == pytest.approx(math.exp(-0.15), rel=1e-15)
+
+
+def test_invalid_hyperparameters_rejected():
+    for bad in (dict(h=0.0), dict(h=1e-3, mu=0.0), dict(h=1e-3, alpha=-1.0),
+                dict(h=1e-3, gamma=-0.1), dict(h=1e-3, eps_stab=-1.0),
+                dict(h=float("nan"))):
+        with pytest.raises(RuntimeError):
+            O.coefficients(O.HParams(**bad))
+
+
+# -------------------------------------------------- closed forms of the step
+
+@pytest.mark.parametrize("gamma", [0.0, 0.7])
+def test_without_friction_is_heavy_ball(gamma):
+    """With mu huge the factors never grow, xi~ = 0 and both half-kicks are
+    the identity.  BACD then is the momentum recursion P_{k+1} = d (P_k - h g),
+    X_{k+1} = X_k + h (P_k - h g) (Section 2: B kick, A drift with the kicked
+    momentum, D damping); for a constant gradient its sums have closed forms.
+    Catches: wrong sign of the kick, drift with P_n instead of P^(B), D missing
+    or applied before the kick."""
+    m, n, steps, h = 5, 7, 40, 0.05
+    rng = _rng(2)
+    x0, p0, g = rng.standard_normal((3, m, n))
+    t = O.make_tensor(x0, p0=p0)
+    hp = O.HParams(h=h, gamma=gamma, alpha=0.3, mu=1e300, eps_stab=1e-8)
+    for _ in range(steps):
+        O.step_list([t], [g], hp)
+    d = math.exp(-gamma * h)
+    N = steps
+    if gamma == 0.0:
+        p_ref = p0 - N * h * g
+        x_ref = x0 + h * (N * p0 - h * g * N * (N + 1) / 2)
+    else:
+        S = (1 - d ** N) / (1 - d)
+        p_ref = d ** N * p0 - h * g * d * S
+        x_ref = x0 + h * (p0 * S - h * g * d * (N - S) / (1 - d) - N * h * g)
+    np.testing.assert_allclose(t.p, p_ref, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(t.x, x_ref, rtol=1e-12, atol=1e-13)
+
+
+def test_factor_filter_closed_form():
+    """With eps_stab huge xi~ vanishes, so with g = 0, gamma = 0 the momentum
+    stays fixed and the factors follow the explicit linear filter of the
+    boundedness lemma's proof (App. convergence analysis):
+    R(t) = e^{-alpha t} R_0 + (1 - e^{-alpha t})/(alpha mu) [P]^2 1_n, and the
+    same with column sums for C.  Catches: rows/columns swapped, wrong decay,
+    wrong forcing scale 1/mu."""
+    m, n, steps = 6, 4, 25
+    rng = _rng(3)
+    x0, p0 = rng.standard_normal((2, m, n))
+    r0, c0 = rng.random(m), rng.random(n)
+    hp = O.HParams(h=0.2, gamma=0.0, alpha=0.35, mu=0.8, eps_stab=1e300)
+    t = O.make_tensor(x0, p0=p0, r0=r0, c0=c0)
+    for _ in range(steps):
+        O.step_list([t], [np.zeros((m, n))], hp)
+    T = steps * hp.h
+    decay = math.exp(-hp.alpha * T)
+    gain = (1 - decay) / (hp.alpha * hp.mu)
+    np.testing.assert_allclose(t.p, p0, rtol=1e-12)
+    np.testing.assert_allclose(t.r, decay * r0 + gain * (p0 ** 2).sum(axis=1), rtol=1e-12)
+    np.testing.assert_allclose(t.c, decay * c0 + gain * (p0 ** 2).sum(axis=0), rtol=1e-12)
+
+
+def test_pure_decay_of_friction():
+    """P = 0, g = 0, eps_stab = 0: the factors only relax, and the rank-1
+    friction decays as xi~(t) = e^{-alpha t} xi~(0) (eqs. rikfad_R, rikfad_C
+    with zero forcing, and eq. xi_def)."""
+    m, n, steps = 7, 3, 30
+    rng = _rng(4)
+    r0, c0 = rng.random(m), rng.random(n)
+    hp = O.HParams(h=0.1, gamma=0.0, alpha=0.6, mu=1.0, eps_stab=0.0)
+    t = O.make_tensor(np.zeros((m, n)), r0=r0, c0=c0)
+    xi0 = O.rank1_friction(r0, c0, 0.0)
+    for _ in range(steps):
+        O.step_list([t], [np.zeros((m, n))], hp)
+    np.testing.assert_allclose(O.rank1_friction(t.r, t.c, 0.0),
+                               math.exp(-hp.alpha * steps * hp.h) * xi0, rtol=1e-13)
+    assert np.all(t.p == 0.0)
+
+
+@pytest.mark.parametrize("eps", [0.0, 0.37])
+def test_rank1_momentum_one_step_closed_form(eps):
+    """From P_0 = u v^T, g = 0, R = C = 0 one step can be written out by hand:
+    xi~_0 = 0 (convention at 1^T R = 0 when eps = 0; R = 0 otherwise), so
+    P^(1) = P_0; R_1 = kappa u^2 |v|^2, C_1 = kappa v^2 |u|^2, S = kappa |u|^2|v|^2,
+    xi~_1 = kappa P_0^2 S/(S + eps).  At eps = 0 this equals the full iKFAD
+    friction (rank-1 identity), checked against the separately written
+    element-wise iKFAD step as well.  Catches: wrong reduction axis, factors
+    driven by the wrong momentum, eps in the wrong place."""
+    m, n = 4, 6
+    rng = _rng(5)
+    u, v = rng.standard_normal(m), rng.standard_normal(n)
+    p0 = np.outer(u, v)
+    hp = O.HParams(h=0.3, gamma=0.2, alpha=0.5, mu=0.25, eps_stab=eps)
+    a, kappa, d = O.coefficients(hp)
+    t = O.make_tensor(np.zeros((m, n)), p0=p0)
+    O.step_list([t], [np.zeros((m, n))], hp)
+    S = kappa * (u @ u) * (v @ v)
+    xi1 = kappa * p0 ** 2 * S / (S + eps)
+    np.testing.assert_allclose(t.r, kappa * u ** 2 * (v @ v), rtol=1e-14)
+    np.testing.assert_allclose(t.c, kappa * v ** 2 * (u @ u), rtol=1e-14)
+    np.testing.assert_allclose(t.p, d * p0 * np.exp(-0.5 * hp.h * xi1), rtol=1e-14)
+    np.testing.assert_allclose(t.x, hp.h * p0, rtol=1e-14)
+    if eps == 0.0:
+        x, p, xi = np.zeros(m * n), p0.ravel().copy(), np.zeros(m * n)
+        O.ikfad_step(x, np.zeros(m * n), p, xi, hp)
+        np.testing.assert_allclose(t.p.ravel(), p, rtol=1e-14)
+        np.testing.assert_allclose(O.rank1_friction(t.r, t.c, 0.0).ravel(), xi, rtol=1e-14)
+
+
+def test_scalar_two_steps_by_hand():
+    """m = n = 1, eps = 0, g = 0, P_0 = 1, R = C = 0, written out over two
+    steps from the Table: step 1 has xi~ = 0 then R_1 = C_1 = kappa, so
+    xi~_1 = kappa and P_1 = d e^{-h kappa/2}.  Step 2 kicks with xi~ = kappa:
+    P^(1) = d e^{-h kappa}; R_2 = kappa (a + d^2 e^{-2 h kappa}) = xi~_2;
+    P_2 = d^2 e^{-h kappa - (h/2) R_2}; X_2 = X_0 + h (1 + P_1).  Catches:
+    factors driven by P^(B) or P^(2) instead of P^(1), half-kick with the
+    wrong factors, D in the wrong place."""
+    hp = O.HParams(h=0.4, gamma=0.3, alpha=0.9, mu=0.5, eps_stab=0.0)
+    a, kappa, d = O.coefficients(hp)
+    h = hp.h
+    t = O.make_tensor(np.array([[0.25]]), p0=np.array([[1.0]]))
+    O.rikfad_matrix_step(t.x, np.zeros((1, 1)), t.p, t.r, t.c, hp)
+    P1 = d * math.exp(-h * kappa / 2)
+    assert t.r[0] == pytest.approx(kappa, rel=1e-15)
+    assert t.p[0, 0] == pytest.approx(P1, rel=1e-15)
+    O.rikfad_matrix_step(t.x, np.zeros((1, 1)), t.p, t.r, t.c, hp)
+    R2 = kappa * (a + d * d * math.exp(-2 * h * kappa))
+    assert t.r[0] == pytest.approx(R2, rel=1e-14)
+    assert t.c[0] == pytest.approx(R2, rel=1e-14)
+    assert t.p[0, 0] == pytest.approx(d * d * math.exp(-h * kappa - 0.5 * h * R2), rel=1e-14)
+    assert t.x[0, 0] == pytest.approx(0.25 + h * (1 + P1), rel=1e-15)
+
+
+# ------------------------------------------------ special cases and identities
+
+@pytest.mark.parametrize("shape", [(1, 9), (11, 1), (1, 1)])
+def test_vector_shapes_reduce_to_elementwise_ikfad(shape):
+    """For m = 1 (or n = 1) and eps_stab = 0, xi~_1j = R_1 C_j / R_1 = C_j and
+    C follows exactly the element-wise iKFAD friction filter, so the rank-1
+    matrix step equals element-wise iKFAD (Section 2, "Memory Complexity":
+    non-2D parameters reduce to element-wise iKFAD).  50 steps with strong
+    friction and fresh gradients."""
+    m, n = shape
+    rng = _rng(6)
+    hp = O.HParams(h=0.1, gamma=0.05, alpha=0.1, mu=0.1, eps_stab=0.0)
+    x0 = rng.standard_normal((m, n)) * 0.02
+    mat = O.make_tensor(x0)
+    xv, pv, xiv = x0.ravel().copy(), np.zeros(m * n), np.zeros(m * n)
+    for s in range(50):
+        g = rng.standard_normal((m, n))
+        O.rikfad_matrix_step(mat.x, g, mat.p, mat.r, mat.c, hp)
+        O.ikfad_step(xv, g.ravel(), pv, xiv, hp)
+    np.testing.assert_allclose(mat.p.ravel(), pv, rtol=1e-12, atol=1e-300)
+    np.testing.assert_allclose(mat.x.ravel(), xv, rtol=1e-12)
+    long = mat.c if m == 1 else mat.r
+    np.testing.assert_allclose(long, xiv, rtol=1e-12)
+    assert np.max(0.5 * hp.h * xiv) > 0.05        # the friction really acted
+
+
+def test_step_list_dispatches_vectors_to_elementwise_ikfad():
+    """A 1 x n tensor in a parameter list keeps its element-wise friction in c
+    and an m x 1 tensor in r; with eps_stab > 0 they follow iKFAD, not the
+    rank-1 formula (which would carry the factor S/(S+eps))."""
+    rng = _rng(7)
+    hp = O.HParams(h=0.1, gamma=0.0, alpha=0.1, mu=0.1, eps_stab=0.5)
+    row = O.make_tensor(rng.standard_normal((1, 8)))
+    col = O.make_tensor(rng.standard_normal((8, 1)))
+    ref = [(t.x.ravel().copy(), t.p.ravel().copy(), np.zeros(8)) for t in (row, col)]
+    for s in range(10):
+        g = rng.standard_normal(8)
+        O.step_list([row, col], [g.reshape(1, 8), g.reshape(8, 1)], hp)
+        for x, p, xi in ref:
+            O.ikfad_step(x, g, p, xi, hp)
+    np.testing.assert_array_equal(row.c, ref[0][2])
+    np.testing.assert_array_equal(col.r, ref[1][2])
+    np.testing.assert_array_equal(row.p.ravel(), ref[0][1])
+    assert np.all(row.r == 0) and np.all(col.c == 0)
+
+
+def _friction_run(m, n, steps, seed, transpose=False, eps=1e-8, gamma=0.0):
+    rng = _rng(seed)
+    s, tcol = rng.lognormal(0, 0.5, m), rng.lognormal(0, 0.5, n)
+    x0 = rng.standard_normal((m, n)) * 0.02
+    gs = [s[:, None] * tcol[None, :] * rng.standard_normal((m, n)) for _ in range(steps)]
+    hp = O.HParams(h=0.1, gamma=gamma, alpha=0.1, mu=0.1, eps_stab=eps)
+    if transpose:
+        x0, gs = x0.T.copy(), [g.T.copy() for g in gs]
+    t = O.make_tensor(x0)
+    hist = []
+    for g in gs:
+        O.step_list([t], [g], hp)
+        hist.append((t.r.copy(), t.c.copy(), O.rank1_friction(t.r, t.c, eps)))
+    return t, hist
+
+
+def test_invariants_nonnegative_balanced_and_bounded():
+    """Lemma (boundedness): R, C >= 0 and 0 <= xi~_ij <= C_j; Lemma (zero-
+    stabiliser phase space): the totals agree, 1^T R = 1^T C, since both obey
+    s' = a s + kappa |P^(1)|_F^2 from R_0 = C_0 = 0.  Catches: a sign error in
+    the forcing, the friction formula using the wrong total."""
+    t, hist = _friction_run(13, 21, 50, seed=8)
+    for r, c, xi in hist:
+        assert np.all(r >= 0) and np.all(c >= 0)
+        assert abs(r.sum() - c.sum()) <= 1e-12 * r.sum()
+        assert np.all(xi >= 0) and np.all(xi <= c[None, :] * (1 + 1e-15))
+    assert np.median(0.5 * 0.1 * hist[-1][2]) > 0.01
+
+
+def test_transpose_invariance():
+    """Running on X^T swaps the roles of R and C and transposes the result;
+    ratio R_i C_j / 1^T R is symmetric because 1^T R = 1^T C."""
+    a, _ = _friction_run(9, 14, 30, seed=9)
+    b, _ = _friction_run(9, 14, 30, seed=9, transpose=True)
+    np.testing.assert_allclose(b.x, a.x.T, rtol=1e-12)
+    np.testing.assert_allclose(b.p, a.p.T, rtol=1e-11)
+    np.testing.assert_allclose(b.r, a.c, rtol=1e-12)
+    np.testing.assert_allclose(b.c, a.r, rtol=1e-12)
+
+
+def test_bf16_parameter_storage():
+    """A bf16 parameter is stored as the nearest bf16 value of the fp64
+    update, and the unrounded update is reported beside it."""
+    rng = _rng(10)
+    x0 = torch.from_numpy(rng.standard_normal((6, 10)).astype(np.float32) * 0.02).to(
+        torch.bfloat16).to(torch.float64).numpy()
+    t = O.make_tensor(x0, bf16=True, track_unrounded=True)
+    g = rng.standard_normal((6, 10))
+    O.step_list([t], [g], O.HParams(h=0.1, alpha=0.1, mu=0.1))
+    np.testing.assert_array_equal(t.x, O.round_bf16(t.x_unrounded))
+    np.testing.assert_allclose(t.x_unrounded, x0 - 0.1 * 0.1 * g, rtol=1e-14)
+
+
+# --------------------------------------------------- quadratic (Section 3)
+
+def _quad(m, n, seed=1):
+    """Section 3 setup: A = B B^T/d + 0.8 I, B standard normal (d = m n);
+    X(0), P(0) normal with standard deviations 0.4 and 0.3; R(0) = C(0) = 0
+    (App. "Numerical Setup")."""
+    rng = _rng(seed)
+    d = m * n
+    B = rng.standard_normal((d, d))
+    A = B @ B.T / d + 0.8 * np.eye(d)
+    return A, rng.standard_normal((m, n)) * 0.4, rng.standard_normal((m, n)) * 0.3
+
+
+def _run_quadratic(m, n, eps, h=0.02, T=1e5, gamma=0.0, seed=1):
+    A, x, p = _quad(m, n, seed)
+    r, c = np.zeros(m), np.zeros(n)
+    every = int(round(1.0 / h))
+    hp = O.HParams(h=h, gamma=gamma, alpha=1.0, mu=1.0, eps_stab=eps)
+    E, worst = O.quadratic_run(A, x, p, r, c, hp, int(round(T / h)), every)
+    t = np.arange(E.size) * every * h
+    return t, E, worst, x
+
+
+def _slope(t, E, lo, hi):
+    sel = (t >= lo) & (t <= hi)
+    return np.polyfit(np.log(t[sel]), np.log(E[sel]), 1)[0]
+
+
+def _gold_slopes():
+    rows = {}
+    for line in open(os.path.join(GOLD, "g0_slopes.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        eps, m, n, *s = line.split()
+        rows[(float(eps), int(m), int(n))] = [float(v) for v in s]
+    return rows
+
+
+@pytest.mark.parametrize("m,n,eps", [(2, 2, 0.0), (2, 2, 0.1), (4, 3, 0.0), (4, 3, 0.1)])
+def test_quadratic_decay_rates(m, n, eps):
+    """Theorem "Algebraic rates": E ~ t^-1 for eps_stab = 0 and E ~ t^-1/2 for
+    eps_stab > 0.  The OLS slope of log E on log t over [1e4, 1e5] must be
+    within 0.03 of the proved exponent and of the paper's Table of local
+    slopes (the paper's random draws differ from ours).  The modified energy
+    f + |P|^2/2 - (h/2)<P, grad f>, conserved exactly by the kick-drift pair
+    on a quadratic, never increases, and X converges to the minimiser 0
+    (Theorem "Convergence when gamma = 0").  Catches a sign error in any
+    friction term (energy growth) and a wrong friction scale (wrong rate)."""
+    t, E, worst, x = _run_quadratic(m, n, eps)
+    s = _slope(t, E, 1e4, 1e5)
+    proved = -1.0 if eps == 0.0 else -0.5
+    paper = _gold_slopes()[(eps, m, n)][1]
+    assert abs(s - proved) < 0.03, s
+    assert abs(s - paper) < 0.03, (s, paper)
+    assert worst <= 1e-12, worst
+    assert np.linalg.norm(x) < 0.05 * 0.4 * math.sqrt(m * n)
+
+
+def test_quadratic_scalar_prefactors():
+    """App. "Prefactor Dependence": for m = n = 1, alpha = mu = 1 at t = 1e5 the
+    paper reports t E/(alpha mu) = 0.909 (eps = 0) and
+    E sqrt(t)/(alpha mu sqrt(eps/2)) = 0.884 (eps > 0; we take eps = 0.1),
+    both near the value 1 of the averaging calculation (Section 3, "Formal
+    rate calculation").  E oscillates, so it is averaged (geometric mean)
+    over [0.9e5, 1e5]; we require agreement with the printed values to 5%."""
+    gold = {}
+    for line in open(os.path.join(GOLD, "scalar_prefactors.txt")):
+        if not line.startswith("#") and line.strip():
+            k, v = line.split()
+            gold[k] = float(v)
+
+    def window(t, E):
+        sel = t >= 0.9e5
+        return math.exp(np.mean(np.log(t[sel]))), math.exp(np.mean(np.log(E[sel])))
+
+    t, E, worst0, _ = _run_quadratic(1, 1, 0.0)
+    tw, Ew = window(t, E)
+    assert tw * Ew == pytest.approx(gold["tE_over_alpha_mu_eps0"], rel=0.05)
+    t, E, worst1, _ = _run_quadratic(1, 1, 0.1)
+    tw, Ew = window(t, E)
+    assert Ew * math.sqrt(tw) / math.sqrt(0.05) == pytest.approx(
+        gold["E_sqrt_t_over_alpha_mu_sqrt_half_eps"], rel=0.05)
+    # For m = n = 1 the friction half-kicks can raise the modified energy by
+    # O(h^2 xi |P| |grad f|) near turning points; it stays negligible.
+    assert max(worst0, worst1) < 1e-6
+
+
+def test_quadratic_step_halving():
+    """App. "Numerical Setup": halving h from 0.02 to 0.01 changed each fitted
+    slope by less than 8.9e-4."""
+    for eps in (0.0, 0.1):
+        ta, Ea, _, _ = _run_quadratic(2, 2, eps, h=0.02)
+        tb, Eb, _, _ = _run_quadratic(2, 2, eps, h=0.01)
+        for lo, hi in ((1e3, 1e4), (1e4, 1e5)):
+            assert abs(_slope(ta, Ea, lo, hi) - _slope(tb, Eb, lo, hi)) < 8.9e-4
+
+
+def test_quadratic_positive_damping_is_exponential():
+    """Theorem "Exponential convergence for gamma > 0": log E falls linearly
+    in t."""
+    t, E, worst, _ = _run_quadratic(3, 2, 1e-8, T=100.0, gamma=0.5)
+    sel = (t >= 10) & (t <= 90)
+    slope, _ = np.polyfit(t[sel], np.log(E[sel]), 1)
+    corr = np.corrcoef(t[sel], np.log(E[sel]))[0, 1]
+    assert slope < -0.2 and corr < -0.999
+    assert worst <= 1e-12
