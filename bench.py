@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the R-iKFAD optimiser step on one MI355X.
+
+Workload: the GPT2-S-shaped parameter set (124,439,808 parameters: 50
+matrices + 98 bias / LayerNorm vectors), seeded synthetic data resident in
+HBM: x ~ N(0, 0.02^2), gradients g_ij = s_i t_j z_ij with log-normal row and
+column scales, p = r = c = 0 at the start.  A step is one rikfad_step over
+all 148 tensors (streaming kernel + finalisation kernel, deferred form).
+
+Prints ONE JSON line.  value = parameters updated per second (whole job);
+roofline = the streaming kernel's compulsory HBM bytes per launch divided
+by its average duration (HIP events recorded by the library around each
+launch on the step's stream) against the 8 TB/s HBM peak; cpu_baseline =
+the fp64 oracle timed on the host cores on a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "optimiser-step params/sec and achieved HBM GB/s (% of peak), GPT2-S-shaped"
+PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "stream_kernel_gpt2s_traffic.json")
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for nm in ("kernels.hip", "layout.hpp", "plan.cpp"):
+        with open(os.path.join(ROOT, "paper_2609_30342_amd", "csrc", nm), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(dtype):
+    """HBM bytes per streaming launch from the committed rocprofv3 counter
+    runs, or None if they were taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    entry = rec.get(dtype)
+    return None if entry is None else entry.get("bytes_per_launch")
+
+
+def build_workload(specs, dtype, seed, device):
+    import torch
+    gen = torch.Generator(device=device).manual_seed(seed)
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xs, gs = [], []
+    for sp in specs:
+        x = (torch.randn((sp.m, sp.n), generator=gen, device=device) * 0.02).to(dt)
+        s = torch.exp(0.5 * torch.randn(sp.m, generator=gen, device=device))
+        t = torch.exp(0.5 * torch.randn(sp.n, generator=gen, device=device))
+        g = (torch.randn((sp.m, sp.n), generator=gen, device=device) * s[:, None]
+             * t[None, :]).to(dt)
+        xs.append(x.contiguous())
+        gs.append(g.contiguous())
+    return xs, gs
+
+
+def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0):
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    dev = torch.device("cuda:0")
+    xs, gs = build_workload(specs, dtype, seed, dev)
+    opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
+    info = opt.query()
+    for _ in range(warmup):
+        opt.step()
+    torch.cuda.synchronize()
+    R.rikfad_timing_enable(opt.ctx, True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        opt.step()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    k1, k2, k3, n = R.rikfad_timing_read(opt.ctx)
+    R.rikfad_timing_enable(opt.ctx, False)
+    nonfinite = opt.nonfinite()
+    opt.close()
+    del xs, gs
+    torch.cuda.empty_cache()
+    return dict(ms_per_step=ms / steps, stream_ms=k1 / n, finalize_ms=k2 / n,
+                apply_ms=k3 / n, info=info, nonfinite=nonfinite)
+
+
+def time_ikfad(specs, hp, steps, warmup, seed=0):
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    xs, gs = build_workload(specs, "fp32", seed, torch.device("cuda:0"))
+    ik = R.IKFAD(xs, gs, h=hp["h"], gamma=hp["gamma"], alpha=hp["alpha"], mu=hp["mu"])
+    for _ in range(warmup):
+        ik.step()
+    torch.cuda.synchronize()
+    R.ikfad_timing_enable(ik.ctx, True)
+    for _ in range(steps):
+        ik.step()
+    ms, n = R.ikfad_timing_read(ik.ctx)
+    ik.close()
+    del xs, gs
+    torch.cuda.empty_cache()
+    return ms / n
+
+
+def time_probe(nfloat, reps=10):
+    """3-read / 2-write fp32 stream of the same byte count as the step."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    bufs = [torch.empty(nfloat, device="cuda:0") for _ in range(5)]
+    for b in bufs[:3]:
+        b.normal_()
+    s = torch.cuda.current_stream().cuda_stream
+    ptrs = [b.data_ptr() for b in bufs]
+    R.rikfad_probe_stream(*ptrs, nfloat, s)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        R.rikfad_probe_stream(*ptrs, nfloat, s)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del bufs
+    torch.cuda.empty_cache()
+    return 20.0 * nfloat / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(specs, hp, budget_s):
+    """The fp64 oracle (as it stands) on a bounded sample of the workload:
+    the position embedding, block 0's four matrices and its eight vectors
+    (7.9M of the 124.4M parameters), stepped until budget_s seconds pass."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2609_30342_amd import synth
+    names = {"wpe"} | {s.name for s in specs if s.name.startswith("h0.")}
+    sample = [s for s in specs if s.name in names]
+    wl = synth.Workload(sample, seed=0)
+    ts = [O.make_tensor(wl.x0(i)) for i in range(len(sample))]
+    grads = [wl.grad(i, 0).astype(np.float64) for i in range(len(sample))]
+    threads = len(os.sched_getaffinity(0))
+    ohp = O.HParams(**hp)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        O.step_list(ts, grads, ohp, threads=threads)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    elems = sum(s.numel for s in sample)
+    return {"value": elems * n / el, "unit": "params/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 oracle, {n} steps over wpe + block 0 of the GPT2-S set "
+                      f"({elems} params, {len(sample)} tensors), OpenMP over tensors, "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--dtype", choices=["fp32", "bf16"], default="fp32")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle time for cpu_baseline (0 = skip)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the bf16 / two-pass / full-iKFAD / probe side measurements")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding is described in DESIGN.md)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2609_30342_amd import synth
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+
+    hp = dict(synth.HP_BASE)
+    specs = synth.gpt2_small(args.dtype)
+    N = sum(s.numel for s in specs)
+    main_run = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup)
+    info = main_run["info"]
+    stream_bytes = info["stream_min_bytes"]
+    achieved = stream_bytes / (main_run["stream_ms"] * 1e-3) / 1e9
+    step_gbps = info["min_bytes_per_step"] / (main_run["ms_per_step"] * 1e-3) / 1e9
+    traffic = measured_traffic(args.dtype)
+    out = {
+        "metric": METRIC,
+        "value": N / (main_run["ms_per_step"] * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_run["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if args.dtype == "fp32" else "bf16 x/g, f32 p/r/c (f32 math)",
+        "data": "synthetic (seeded; GPT2-S shapes, random gradients)",
+        "config": {
+            "workload": f"GPT2-S-shaped parameter set, {args.dtype} x/g: {N} params "
+                        f"({info['matrices']} matrices + {info['vectors']} vectors), "
+                        "deferred single-pass step",
+            "params": N,
+            "hparams": hp,
+            "stream_tiles": info["stream_tiles"],
+            "finalize_items": info["finalize_items"],
+        },
+        "hbm_gbps_step": step_gbps,
+        "hbm_frac_step": step_gbps / PEAK_GBPS,
+        "kernel_ms": {"stream": main_run["stream_ms"], "finalize": main_run["finalize_ms"]},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_GBPS,
+            "traffic": traffic,
+            "kernel": "rikfad_stream_kernel",
+            "bytes_per_launch": stream_bytes,
+        },
+        "state_bytes": {"rikfad": info["state_bytes"], "ikfad": info["ikfad_state_bytes"]},
+        "nonfinite": main_run["nonfinite"],
+    }
+    if not args.no_variants:
+        var = {}
+        other = "bf16" if args.dtype == "fp32" else "fp32"
+        r2 = time_rikfad(synth.gpt2_small(other), other, hp, args.steps, args.warmup)
+        var[f"rikfad_{other}"] = {
+            "ms_per_step": r2["ms_per_step"], "params_per_s": N / (r2["ms_per_step"] * 1e-3),
+            "stream_ms": r2["stream_ms"],
+            "stream_gbps": r2["info"]["stream_min_bytes"] / (r2["stream_ms"] * 1e-3) / 1e9}
+        tp = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup, two_pass=True)
+        var["rikfad_two_pass"] = {"ms_per_step": tp["ms_per_step"],
+                                  "params_per_s": N / (tp["ms_per_step"] * 1e-3)}
+        if args.dtype == "fp32":
+            ik_ms = time_ikfad(specs, hp, args.steps, args.warmup)
+            var["ikfad_full_fp32"] = {"ms_per_step": ik_ms, "params_per_s": N / (ik_ms * 1e-3),
+                                      "hbm_gbps": 28.0 * N / (ik_ms * 1e-3) / 1e9,
+                                      "state_bytes": info["ikfad_state_bytes"]}
+        var["probe_3r2w_gbps"] = time_probe(N)
+        out["variants"] = var
+    if args.cpu_budget > 0:
+        out["cpu_baseline"] = cpu_baseline(specs, hp, args.cpu_budget)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,240 @@
+/*
+ * rikfad.h -- C ABI of the MI355X (gfx950) R-iKFAD optimiser step.
+ *
+ * Method: Rank-1 iKFAD (R. Rajpal, B. Leimkuhler, "Low-Rank Friction for
+ * Memory-Efficient Transformer Pretraining").  For every weight matrix
+ * X (m x n) with momentum P (m x n) and friction factors R (m), C (n), one
+ * optimiser step is the BACD splitting of Section 2 ("Splitting
+ * Discretization"), written out in App. A (Table of analytical sub-step
+ * updates):
+ *
+ *   B    P^(B)   = P_n - h g                       (g = gradient at X_n)
+ *   A    X_{n+1} = X_n + h P^(B)
+ *   C.1  xi~_n   = R_n C_n^T / (1^T R_n + eps_stab)          eq. (xi_def)
+ *        P^(1)   = P^(B) .* exp(-(h/2) xi~_n)
+ *   C.2  R_{n+1} = e^{-alpha h} R_n + (1 - e^{-alpha h})/(mu alpha) [P^(1)]^2 1_n
+ *   C.3  C_{n+1} = e^{-alpha h} C_n + (1 - e^{-alpha h})/(mu alpha) ([P^(1)]^2)^T 1_m
+ *   C.4  P^(2)   = P^(1) .* exp(-(h/2) xi~_{n+1})
+ *   D    P_{n+1} = P^(2) e^{-gamma h}
+ *
+ * with xi~ = 0 when 1^T R + eps_stab == 0 (the eps_stab = 0 convention of
+ * Theorem "Algebraic rates").  Tensors with m == 1 or n == 1 (biases,
+ * LayerNorm scales) take element-wise iKFAD instead (Section 2, "Memory
+ * Complexity"): the same steps with one friction entry per parameter,
+ * xi_{n+1} = e^{-alpha h} xi_n + (1 - e^{-alpha h})/(mu alpha) [P^(1)]^2.
+ *
+ * All entry points are asynchronous on the HIP stream they are given
+ * (a hipStream_t passed as void*; NULL is the default stream) unless stated
+ * otherwise, return a rikfad_status, and never throw.  A context is not
+ * thread-safe; distinct contexts are independent.
+ */
+#ifndef RIKFAD_H
+#define RIKFAD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RIKFAD_OK = 0,
+    RIKFAD_EINVAL = -1,     /* bad argument (NULL, size, hyperparameter) */
+    RIKFAD_EALIGN = -2,     /* a pointer is not aligned to its element type */
+    RIKFAD_EDTYPE = -3,     /* unsupported dtype code */
+    RIKFAD_ENOMEM = -4,     /* host or device allocation failed */
+    RIKFAD_EHIP = -5,       /* a HIP runtime call or kernel launch failed */
+    RIKFAD_ESTATE = -6      /* call not valid in the context's current state */
+} rikfad_status;
+
+/* Storage type of x and g.  p, r, c (and xi) are always fp32. */
+typedef enum { RIKFAD_FP32 = 0, RIKFAD_BF16 = 1 } rikfad_dtype;
+
+/* One parameter tensor: all pointers are device pointers, row-major and
+ * contiguous (row i, column j at offset i*n + j).
+ *   x  m*n elements of `dtype`, the parameter X, updated in place.  A bf16
+ *      parameter is computed in fp32 and stored rounded to nearest-even.
+ *   g  m*n elements of `dtype`, the gradient at the current X; read only.
+ *   p  m*n fp32, the momentum (see the deferred form below).
+ *   r  m fp32, c  n fp32: the friction factors R and C.
+ * Vectors (m == 1 or n == 1) keep their element-wise friction (m*n entries)
+ * in c when m == 1 and in r otherwise; the other factor is unused and may be
+ * NULL.  The caller owns every buffer, keeps it alive and in place from
+ * create to destroy, zero-fills p, r and c before the first step (the paper
+ * starts from R = C = 0) unless it resumes a saved state, and never lets two
+ * tensors of one context share memory.  Every pointer must be aligned to its
+ * element size; 16-byte alignment (and n a multiple of 4 for fp32, of 8 for
+ * bf16) selects the 128-bit load path, anything else a scalar path. */
+typedef struct {
+    void *x;
+    const void *g;
+    float *p;
+    float *r;
+    float *c;
+    int64_t m, n;
+    int32_t dtype;          /* rikfad_dtype */
+    int32_t reserved;       /* must be 0 */
+} rikfad_tensor;
+
+/* Hyperparameters shared by all tensors of a context (the paper tunes them
+ * per model, App. "Optimal Hyperparameters").  Requirements: h > 0, mu > 0,
+ * alpha >= 0 (alpha = 0 takes the limit (1 - e^{-alpha h})/(mu alpha) ->
+ * h/mu), gamma >= 0 (0 is R-iKFAD0), eps_stab >= 0, all finite.  The step
+ * uses them as fp32 after computing e^{-alpha h}, the factor gain,
+ * e^{-gamma h} and h/2 in fp64 on the host. */
+typedef struct {
+    double h, gamma, alpha, mu, eps_stab;
+} rikfad_hparams;
+
+typedef struct rikfad_ctx rikfad_ctx;
+
+/* Flags for rikfad_create. */
+#define RIKFAD_FLAG_TWO_PASS 1u   /* p holds P_{n+1} after every step */
+
+/* Create a context over `count` tensors (count >= 0; 0 gives a context whose
+ * step does nothing).  Validates every argument before any HIP call, builds
+ * the device tile tables and allocates the reduction workspace (about
+ * 8 (m + n) bytes per matrix plus 4 m n/256 bytes of partial sums) on the
+ * current HIP device.  The tensor array is copied; the buffers it points to
+ * are not.  Zero-size tensors (m < 1 or n < 1) are rejected with
+ * RIKFAD_EINVAL.
+ *
+ * Deferred form (default).  The second friction half-kick and D of step n
+ * use the same factor R_{n+1}, C_{n+1} as the first half-kick of step n+1,
+ * so the library applies them at the start of step n+1 inside the same
+ * streaming pass: between steps a matrix's p holds P^(1) of the last step
+ * and the step moves the minimum number of bytes (read x, g, p; write x, p).
+ * X, R and C are always those of the paper's step.  Call
+ * rikfad_sync_momentum to turn p into P_{n+1} (before reading p or saving a
+ * checkpoint).  Vector tensors are never deferred.
+ * RIKFAD_FLAG_TWO_PASS instead applies the second half-kick in a separate
+ * pass after every step, so p always holds P_{n+1} (28 bytes per fp32
+ * parameter instead of 20). */
+rikfad_status rikfad_create(const rikfad_tensor *tensors, int64_t count,
+                            const rikfad_hparams *hp, uint32_t flags,
+                            rikfad_ctx **out);
+
+/* Enqueue one optimiser step on `stream`, reading the gradients g given at
+ * create (or at the last rikfad_step_grads).  Three kernels at most: the
+ * fused streaming pass over all tensors (B, A, C.1, the deferred C.4 + D,
+ * per-tile row and column partial sums of [P^(1)]^2), the fixed-order
+ * finalisation of R, C and 1^T R, and in two-pass mode the C.4 + D pass.
+ * Results are bitwise reproducible: no atomics, fixed reduction order. */
+rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream);
+
+/* As rikfad_step, with new gradient pointers grads[0..count-1] (same shapes,
+ * dtypes and alignment class as at create; RIKFAD_EALIGN otherwise).  For
+ * frameworks that reallocate gradients between steps. */
+rikfad_status rikfad_step_grads(rikfad_ctx *ctx, const void *const *grads,
+                                void *stream);
+
+/* Replace the hyperparameters.  If a deferred half-kick is pending and h,
+ * gamma or eps_stab change, the pending half-kick (which belongs to the
+ * previous step and its hyperparameters) is applied first on `stream`. */
+rikfad_status rikfad_set_hparams(rikfad_ctx *ctx, const rikfad_hparams *hp,
+                                 void *stream);
+
+/* Apply a pending deferred half-kick so that every p holds P_{n+1}
+ * (App. A Table rows C.4 and D).  No-op when nothing is pending. */
+rikfad_status rikfad_sync_momentum(rikfad_ctx *ctx, void *stream);
+
+/* Tell the context that the caller rewrote p, r or c (e.g. restored a
+ * checkpoint saved after rikfad_sync_momentum): p is taken to hold P_n, no
+ * half-kick is pending, and 1^T R is recomputed before the next step. */
+rikfad_status rikfad_state_changed(rikfad_ctx *ctx);
+
+typedef struct {
+    int64_t tensors, matrices, vectors;
+    int64_t elements;          /* sum of m n */
+    int64_t state_bytes;       /* optimiser state p, r, c (and vector xi) */
+    int64_t ikfad_state_bytes; /* the same model under full iKFAD: 8 m n */
+    int64_t workspace_bytes;   /* device memory owned by the context */
+    int64_t min_bytes_per_step;/* compulsory HBM traffic of one step: per
+                                  matrix element read x, g, p and write x, p
+                                  (20 B fp32, 14 B bf16 x/g), plus R and C read
+                                  and written; per vector element also xi */
+    int64_t stream_min_bytes;  /* the same for the streaming kernel alone
+                                  (R, C read, not written) */
+    int64_t stream_tiles;      /* workgroups of the streaming pass */
+    int64_t finalize_items;    /* workgroups of the finalisation pass */
+    int32_t pending;           /* 1 if a deferred half-kick is pending */
+    int32_t two_pass;
+} rikfad_info;
+
+/* Describe a context (host only, no HIP call). */
+rikfad_status rikfad_query(const rikfad_ctx *ctx, rikfad_info *out);
+
+/* Host-only accounting of a tensor list, no HIP call: R-iKFAD optimiser
+ * state (4 m n for p plus 4 (m + n) for R, C per matrix; 8 m n per vector)
+ * and full iKFAD state (8 m n) in bytes.  App. "Memory Analysis" reports
+ * these as N + sum (m + n) versus 2N scalars. */
+rikfad_status rikfad_state_bytes(const rikfad_tensor *tensors, int64_t count,
+                                 int64_t *rikfad_bytes, int64_t *ikfad_bytes);
+
+/* Blocking: wait for `stream`, then report whether any finalised factor
+ * (R, C or their sum) has been non-finite since create (1) or not (0).
+ * Non-finite values are propagated, never masked. */
+rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out);
+
+/* Kernel timing with HIP events recorded on the step's stream around each
+ * kernel of every subsequent step (enable != 0), for benchmarks.
+ * rikfad_timing_read waits for the last recorded event and returns the
+ * summed milliseconds of the streaming, finalisation and two-pass kernels
+ * and the number of timed steps, then clears the record. */
+rikfad_status rikfad_timing_enable(rikfad_ctx *ctx, int32_t enable);
+rikfad_status rikfad_timing_read(rikfad_ctx *ctx, double *stream_ms,
+                                 double *finalize_ms, double *apply_ms,
+                                 int64_t *steps);
+
+void rikfad_destroy(rikfad_ctx *ctx);
+
+const char *rikfad_status_string(rikfad_status s);
+
+/* Message describing the most recent failure on the calling thread. */
+const char *rikfad_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Full-tensor iKFAD (comparison point).  Section 1, iKFAD dynamics, with
+ * the same BACD splitting and sub-flow C treatment as above, one friction
+ * entry per parameter: reads x, g, p, xi and writes x, p, xi (28 bytes per
+ * fp32 parameter) and keeps 2N state scalars against R-iKFAD's
+ * N + sum(m + n).  Same conventions as the R-iKFAD entry points.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    void *x;
+    const void *g;
+    float *p;
+    float *xi;              /* m*n fp32 friction */
+    int64_t m, n;
+    int32_t dtype;
+    int32_t reserved;
+} ikfad_tensor;
+
+typedef struct ikfad_ctx ikfad_ctx;
+
+rikfad_status ikfad_create(const ikfad_tensor *tensors, int64_t count,
+                           const rikfad_hparams *hp, ikfad_ctx **out);
+rikfad_status ikfad_step(ikfad_ctx *ctx, void *stream);
+rikfad_status ikfad_set_hparams(ikfad_ctx *ctx, const rikfad_hparams *hp);
+rikfad_status ikfad_timing_enable(ikfad_ctx *ctx, int32_t enable);
+rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps);
+void ikfad_destroy(ikfad_ctx *ctx);
+
+/* ------------------------------------------------------------------------
+ * Bandwidth probes (measurement aids for the HBM roofline).
+ *   rikfad_probe_stream: d[i] = a[i] + b[i], e[i] = a[i] * c[i] over nfloat
+ *     fp32 elements -- the 3-read / 2-write mix of the fp32 step, with no
+ *     other work.  All five pointers 16-byte aligned, nfloat % 4 == 0.
+ *   rikfad_probe_copy: dst[i] = src[i] over nbytes (16-byte aligned,
+ *     nbytes % 16 == 0), a plain copy of known size for calibrating
+ *     hardware byte counters.
+ * ---------------------------------------------------------------------- */
+rikfad_status rikfad_probe_stream(const float *a, const float *b, const float *c,
+                                  float *d, float *e, int64_t nfloat, void *stream);
+rikfad_status rikfad_probe_copy(const void *src, void *dst, int64_t nbytes,
+                                void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

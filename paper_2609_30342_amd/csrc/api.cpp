@@ -1,0 +1,534 @@
+// api.cpp -- the extern "C" entry points declared in include/rikfad.h.
+//
+// Host side of the library: argument validation (before any HIP call),
+// device tables, workspace, the deferred half-kick state machine, event
+// timing.  All launches go to the caller's stream; nothing here blocks
+// except the calls documented as blocking.
+#include <hip/hip_runtime_api.h>
+
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/rikfad.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rikfad_status fail(rikfad_status s, const std::string &msg)
+{
+    g_last_error = msg;
+    return s;
+}
+
+rikfad_status hip_fail(hipError_t e, const char *what)
+{
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return RIKFAD_EHIP;
+}
+
+#define HIP_TRY(expr, what)                                   \
+    do {                                                      \
+        hipError_t e_ = (expr);                               \
+        if (e_ != hipSuccess) return hip_fail(e_, what);      \
+    } while (0)
+
+// Device copies of the plan tables plus the partial-sum workspace.
+struct DeviceTables {
+    rk::TensorDesc *tensors = nullptr;
+    const void **grads = nullptr;
+    rk::Tile *tiles = nullptr;
+    rk::FinItem *fin = nullptr;
+    float *ws = nullptr;
+    int *flag = nullptr;
+};
+
+template <typename T>
+rikfad_status upload(T **dst, const std::vector<T> &src, const char *what)
+{
+    if (src.empty()) return RIKFAD_OK;
+    const size_t bytes = sizeof(T) * src.size();
+    HIP_TRY(hipMalloc(reinterpret_cast<void **>(dst), bytes), what);
+    HIP_TRY(hipMemcpy(*dst, src.data(), bytes, hipMemcpyHostToDevice), what);
+    return RIKFAD_OK;
+}
+
+void free_tables(DeviceTables &d)
+{
+    if (d.tensors) (void)hipFree(d.tensors);
+    if (d.grads) (void)hipFree(const_cast<void **>(d.grads));
+    if (d.tiles) (void)hipFree(d.tiles);
+    if (d.fin) (void)hipFree(d.fin);
+    if (d.ws) (void)hipFree(d.ws);
+    if (d.flag) (void)hipFree(d.flag);
+    d = DeviceTables{};
+}
+
+rikfad_status make_tables(const rk::Plan &pl, DeviceTables &d)
+{
+    rikfad_status s;
+    if ((s = upload(&d.tensors, pl.tensors, "hipMalloc/copy tensor table")) != RIKFAD_OK) return s;
+    if ((s = upload(&d.grads, pl.grads, "hipMalloc/copy gradient table")) != RIKFAD_OK) return s;
+    if ((s = upload(&d.tiles, pl.tiles, "hipMalloc/copy tile table")) != RIKFAD_OK) return s;
+    if ((s = upload(&d.fin, pl.fin, "hipMalloc/copy finalisation table")) != RIKFAD_OK) return s;
+    const size_t wsb = sizeof(float) * static_cast<size_t>(pl.ws_floats > 0 ? pl.ws_floats : 1);
+    HIP_TRY(hipMalloc(reinterpret_cast<void **>(&d.ws), wsb), "hipMalloc workspace");
+    HIP_TRY(hipMemset(d.ws, 0, wsb), "hipMemset workspace");
+    HIP_TRY(hipMalloc(reinterpret_cast<void **>(&d.flag), sizeof(int)), "hipMalloc flag");
+    HIP_TRY(hipMemset(d.flag, 0, sizeof(int)), "hipMemset flag");
+    return RIKFAD_OK;
+}
+
+// Gradient-pointer updates go through a small ring of pinned host slots so
+// that the asynchronous copy never reads a buffer the host has reused.
+struct GradRing {
+    static constexpr int kSlots = 4;
+    const void **host[kSlots] = {};
+    hipEvent_t done[kSlots] = {};
+    bool used[kSlots] = {};
+    int next = 0;
+    size_t count = 0;
+
+    rikfad_status init(size_t n)
+    {
+        count = n;
+        for (int i = 0; i < kSlots; ++i) {
+            HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&host[i]),
+                                  sizeof(void *) * (n ? n : 1), hipHostMallocDefault),
+                    "hipHostMalloc gradient slots");
+            HIP_TRY(hipEventCreateWithFlags(&done[i], hipEventDisableTiming), "hipEventCreate");
+        }
+        return RIKFAD_OK;
+    }
+    void release()
+    {
+        for (int i = 0; i < kSlots; ++i) {
+            if (host[i]) (void)hipHostFree(host[i]);
+            if (done[i]) (void)hipEventDestroy(done[i]);
+            host[i] = nullptr;
+            done[i] = nullptr;
+        }
+    }
+    rikfad_status push(const void **dev, const void *const *src, hipStream_t stream)
+    {
+        const int s = next;
+        next = (next + 1) % kSlots;
+        if (used[s]) HIP_TRY(hipEventSynchronize(done[s]), "hipEventSynchronize gradient slot");
+        std::memcpy(host[s], src, sizeof(void *) * count);
+        HIP_TRY(hipMemcpyAsync(dev, host[s], sizeof(void *) * count, hipMemcpyHostToDevice, stream),
+                "hipMemcpyAsync gradient table");
+        HIP_TRY(hipEventRecord(done[s], stream), "hipEventRecord gradient slot");
+        used[s] = true;
+        return RIKFAD_OK;
+    }
+};
+
+// Per-step event timing (benchmarks only).
+struct Timing {
+    bool on = false;
+    std::vector<hipEvent_t> ev;     // 4 per step: before, after stream, after finalize, after apply
+    int64_t steps = 0;
+
+    rikfad_status mark(int64_t step, int slot, hipStream_t stream)
+    {
+        const size_t idx = static_cast<size_t>(step * 4 + slot);
+        while (ev.size() <= idx) {
+            hipEvent_t e;
+            HIP_TRY(hipEventCreate(&e), "hipEventCreate timing");
+            ev.push_back(e);
+        }
+        HIP_TRY(hipEventRecord(ev[idx], stream), "hipEventRecord timing");
+        return RIKFAD_OK;
+    }
+    void release()
+    {
+        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+        ev.clear();
+    }
+};
+
+}  // namespace
+
+struct rikfad_ctx {
+    rk::Plan plan;
+    DeviceTables dev;
+    GradRing ring;
+    Timing timing;
+    rikfad_hparams hp{};
+    rk::Coeffs k{};
+    bool two_pass = false;
+    bool pending = false;       // a deferred C.4 + D is owed to the matrices' p
+    bool sums_valid = false;    // partial sums of R reflect the current R
+    std::vector<const void *> grads_host;
+};
+
+struct ikfad_ctx {
+    rk::Plan plan;
+    DeviceTables dev;
+    Timing timing;
+    rikfad_hparams hp{};
+    rk::Coeffs k{};
+};
+
+extern "C" {
+
+const char *rikfad_status_string(rikfad_status s)
+{
+    switch (s) {
+    case RIKFAD_OK: return "ok";
+    case RIKFAD_EINVAL: return "invalid argument";
+    case RIKFAD_EALIGN: return "misaligned pointer";
+    case RIKFAD_EDTYPE: return "unsupported dtype";
+    case RIKFAD_ENOMEM: return "out of memory";
+    case RIKFAD_EHIP: return "HIP runtime error";
+    case RIKFAD_ESTATE: return "invalid state";
+    }
+    return "unknown status";
+}
+
+const char *rikfad_last_error(void) { return g_last_error.c_str(); }
+
+rikfad_status rikfad_state_bytes(const rikfad_tensor *tensors, int64_t count,
+                                 int64_t *rikfad_bytes, int64_t *ikfad_bytes)
+{
+    if (!rikfad_bytes || !ikfad_bytes) return fail(RIKFAD_EINVAL, "output pointer is NULL");
+    rk::Plan pl;
+    std::string err;
+    rikfad_status s = rk::plan_rikfad(tensors, count, pl, err);
+    if (s != RIKFAD_OK) return fail(s, err);
+    *rikfad_bytes = pl.state_bytes;
+    *ikfad_bytes = pl.ikfad_state_bytes;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_create(const rikfad_tensor *tensors, int64_t count,
+                            const rikfad_hparams *hp, uint32_t flags, rikfad_ctx **out)
+{
+    if (!out) return fail(RIKFAD_EINVAL, "out is NULL");
+    *out = nullptr;
+    std::string err;
+    if (flags & ~RIKFAD_FLAG_TWO_PASS) return fail(RIKFAD_EINVAL, "unknown flag bits");
+    rikfad_status s = rk::check_hparams(hp, err);
+    if (s != RIKFAD_OK) return fail(s, err);
+    rikfad_ctx *ctx = new (std::nothrow) rikfad_ctx();
+    if (!ctx) return fail(RIKFAD_ENOMEM, "host allocation failed");
+    s = rk::plan_rikfad(tensors, count, ctx->plan, err);
+    if (s != RIKFAD_OK) {
+        delete ctx;
+        return fail(s, err);
+    }
+    ctx->hp = *hp;
+    ctx->k = rk::make_coeffs(*hp);
+    ctx->two_pass = (flags & RIKFAD_FLAG_TWO_PASS) != 0;
+    ctx->grads_host = ctx->plan.grads;
+    if ((s = make_tables(ctx->plan, ctx->dev)) != RIKFAD_OK ||
+        (s = ctx->ring.init(ctx->plan.grads.size())) != RIKFAD_OK) {
+        std::string keep = g_last_error;
+        free_tables(ctx->dev);
+        ctx->ring.release();
+        delete ctx;
+        g_last_error = keep;
+        return s;
+    }
+    *out = ctx;
+    return RIKFAD_OK;
+}
+
+static rikfad_status apply_pending(rikfad_ctx *ctx, hipStream_t stream)
+{
+    if (!ctx->pending) return RIKFAD_OK;
+    hipError_t e = rk::launch_apply(ctx->dev.tensors, ctx->dev.tiles, ctx->plan.matrix_tiles,
+                                    ctx->dev.ws, ctx->k, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch apply kernel");
+    ctx->pending = false;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    hipStream_t stream = static_cast<hipStream_t>(stream_);
+    const rk::Plan &pl = ctx->plan;
+    if (pl.tiles.empty()) return RIKFAD_OK;
+    hipError_t e;
+    if (!ctx->sums_valid && pl.row_items > 0) {
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, pl.row_items, ctx->dev.ws, ctx->k,
+                                ctx->dev.flag, 1, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (init)");
+    }
+    ctx->sums_valid = true;
+    Timing &tm = ctx->timing;
+    rikfad_status s;
+    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    e = rk::launch_stream(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
+                          static_cast<int64_t>(pl.tiles.size()), ctx->dev.ws, ctx->k,
+                          ctx->pending ? 1 : 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
+    ctx->pending = false;
+    if (tm.on && (s = tm.mark(tm.steps, 1, stream)) != RIKFAD_OK) return s;
+    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, static_cast<int64_t>(pl.fin.size()),
+                            ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
+    if (tm.on && (s = tm.mark(tm.steps, 2, stream)) != RIKFAD_OK) return s;
+    ctx->pending = pl.matrix_tiles > 0;
+    if (ctx->two_pass && (s = apply_pending(ctx, stream)) != RIKFAD_OK) return s;
+    if (tm.on) {
+        if ((s = tm.mark(tm.steps, 3, stream)) != RIKFAD_OK) return s;
+        tm.steps += 1;
+    }
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_step_grads(rikfad_ctx *ctx, const void *const *grads, void *stream)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    const size_t n = ctx->plan.tensors.size();
+    if (n > 0 && !grads) return fail(RIKFAD_EINVAL, "grads is NULL");
+    bool changed = false;
+    for (size_t i = 0; i < n; ++i) {
+        const rk::TensorDesc &d = ctx->plan.tensors[i];
+        if (!rk::grad_fits(grads[i], d.dtype, d.vec))
+            return fail(grads[i] ? RIKFAD_EALIGN : RIKFAD_EINVAL,
+                        "gradient " + std::to_string(i) +
+                            " is NULL or breaks the alignment planned at create");
+        changed = changed || grads[i] != ctx->grads_host[i];
+    }
+    if (changed) {
+        rikfad_status s = ctx->ring.push(ctx->dev.grads, grads, static_cast<hipStream_t>(stream));
+        if (s != RIKFAD_OK) return s;
+        for (size_t i = 0; i < n; ++i) ctx->grads_host[i] = grads[i];
+    }
+    return rikfad_step(ctx, stream);
+}
+
+rikfad_status rikfad_set_hparams(rikfad_ctx *ctx, const rikfad_hparams *hp, void *stream)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    std::string err;
+    rikfad_status s = rk::check_hparams(hp, err);
+    if (s != RIKFAD_OK) return fail(s, err);
+    const bool kick_changes = hp->h != ctx->hp.h || hp->gamma != ctx->hp.gamma ||
+                              hp->eps_stab != ctx->hp.eps_stab;
+    if (ctx->pending && kick_changes &&
+        (s = apply_pending(ctx, static_cast<hipStream_t>(stream))) != RIKFAD_OK)
+        return s;
+    ctx->hp = *hp;
+    ctx->k = rk::make_coeffs(*hp);
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_sync_momentum(rikfad_ctx *ctx, void *stream)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    return apply_pending(ctx, static_cast<hipStream_t>(stream));
+}
+
+rikfad_status rikfad_state_changed(rikfad_ctx *ctx)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    ctx->pending = false;
+    ctx->sums_valid = false;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_query(const rikfad_ctx *ctx, rikfad_info *out)
+{
+    if (!ctx || !out) return fail(RIKFAD_EINVAL, "ctx or out is NULL");
+    const rk::Plan &pl = ctx->plan;
+    rikfad_info info{};
+    info.tensors = static_cast<int64_t>(pl.tensors.size());
+    info.matrices = pl.matrices;
+    info.vectors = pl.vectors;
+    info.elements = pl.elements;
+    info.state_bytes = pl.state_bytes;
+    info.ikfad_state_bytes = pl.ikfad_state_bytes;
+    info.workspace_bytes = static_cast<int64_t>(
+        4 * pl.ws_floats + sizeof(int) + sizeof(rk::TensorDesc) * pl.tensors.size() +
+        sizeof(void *) * pl.grads.size() + sizeof(rk::Tile) * pl.tiles.size() +
+        sizeof(rk::FinItem) * pl.fin.size());
+    info.min_bytes_per_step = pl.min_bytes;
+    info.stream_min_bytes = pl.stream_min_bytes;
+    info.stream_tiles = static_cast<int64_t>(pl.tiles.size());
+    info.finalize_items = static_cast<int64_t>(pl.fin.size());
+    info.pending = ctx->pending ? 1 : 0;
+    info.two_pass = ctx->two_pass ? 1 : 0;
+    *out = info;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out)
+{
+    if (!ctx || !out) return fail(RIKFAD_EINVAL, "ctx or out is NULL");
+    HIP_TRY(hipStreamSynchronize(static_cast<hipStream_t>(stream)), "hipStreamSynchronize");
+    int v = 0;
+    HIP_TRY(hipMemcpy(&v, ctx->dev.flag, sizeof(int), hipMemcpyDeviceToHost), "hipMemcpy flag");
+    *out = v ? 1 : 0;
+    return RIKFAD_OK;
+}
+
+static rikfad_status read_timing(Timing &tm, double *ms3, int64_t *steps)
+{
+    ms3[0] = ms3[1] = ms3[2] = 0.0;
+    if (tm.steps > 0) {
+        HIP_TRY(hipEventSynchronize(tm.ev[static_cast<size_t>(tm.steps * 4 - 1)]),
+                "hipEventSynchronize timing");
+        for (int64_t s = 0; s < tm.steps; ++s) {
+            for (int k = 0; k < 3; ++k) {
+                float ms = 0.f;
+                HIP_TRY(hipEventElapsedTime(&ms, tm.ev[static_cast<size_t>(s * 4 + k)],
+                                            tm.ev[static_cast<size_t>(s * 4 + k + 1)]),
+                        "hipEventElapsedTime");
+                ms3[k] += ms;
+            }
+        }
+    }
+    *steps = tm.steps;
+    tm.steps = 0;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_timing_enable(rikfad_ctx *ctx, int32_t enable)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    ctx->timing.on = enable != 0;
+    ctx->timing.steps = 0;
+    return RIKFAD_OK;
+}
+
+rikfad_status rikfad_timing_read(rikfad_ctx *ctx, double *stream_ms, double *finalize_ms,
+                                 double *apply_ms, int64_t *steps)
+{
+    if (!ctx || !stream_ms || !finalize_ms || !apply_ms || !steps)
+        return fail(RIKFAD_EINVAL, "NULL argument");
+    double ms[3];
+    rikfad_status s = read_timing(ctx->timing, ms, steps);
+    if (s != RIKFAD_OK) return s;
+    *stream_ms = ms[0];
+    *finalize_ms = ms[1];
+    *apply_ms = ms[2];
+    return RIKFAD_OK;
+}
+
+void rikfad_destroy(rikfad_ctx *ctx)
+{
+    if (!ctx) return;
+    free_tables(ctx->dev);
+    ctx->ring.release();
+    ctx->timing.release();
+    delete ctx;
+}
+
+// ------------------------------------------------------------ full iKFAD
+
+rikfad_status ikfad_create(const ikfad_tensor *tensors, int64_t count, const rikfad_hparams *hp,
+                           ikfad_ctx **out)
+{
+    if (!out) return fail(RIKFAD_EINVAL, "out is NULL");
+    *out = nullptr;
+    std::string err;
+    rikfad_status s = rk::check_hparams(hp, err);
+    if (s != RIKFAD_OK) return fail(s, err);
+    ikfad_ctx *ctx = new (std::nothrow) ikfad_ctx();
+    if (!ctx) return fail(RIKFAD_ENOMEM, "host allocation failed");
+    if ((s = rk::plan_ikfad(tensors, count, ctx->plan, err)) != RIKFAD_OK) {
+        delete ctx;
+        return fail(s, err);
+    }
+    ctx->hp = *hp;
+    ctx->k = rk::make_coeffs(*hp);
+    if ((s = make_tables(ctx->plan, ctx->dev)) != RIKFAD_OK) {
+        std::string keep = g_last_error;
+        free_tables(ctx->dev);
+        delete ctx;
+        g_last_error = keep;
+        return s;
+    }
+    *out = ctx;
+    return RIKFAD_OK;
+}
+
+rikfad_status ikfad_step(ikfad_ctx *ctx, void *stream_)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    hipStream_t stream = static_cast<hipStream_t>(stream_);
+    if (ctx->plan.tiles.empty()) return RIKFAD_OK;
+    Timing &tm = ctx->timing;
+    rikfad_status s;
+    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    hipError_t e = rk::launch_ikfad(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
+                                    static_cast<int64_t>(ctx->plan.tiles.size()), ctx->k, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch ikfad kernel");
+    if (tm.on) {
+        for (int k = 1; k < 4; ++k)
+            if ((s = tm.mark(tm.steps, k, stream)) != RIKFAD_OK) return s;
+        tm.steps += 1;
+    }
+    return RIKFAD_OK;
+}
+
+rikfad_status ikfad_set_hparams(ikfad_ctx *ctx, const rikfad_hparams *hp)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    std::string err;
+    rikfad_status s = rk::check_hparams(hp, err);
+    if (s != RIKFAD_OK) return fail(s, err);
+    ctx->hp = *hp;
+    ctx->k = rk::make_coeffs(*hp);
+    return RIKFAD_OK;
+}
+
+rikfad_status ikfad_timing_enable(ikfad_ctx *ctx, int32_t enable)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    ctx->timing.on = enable != 0;
+    ctx->timing.steps = 0;
+    return RIKFAD_OK;
+}
+
+rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps)
+{
+    if (!ctx || !ms || !steps) return fail(RIKFAD_EINVAL, "NULL argument");
+    double t[3];
+    rikfad_status s = read_timing(ctx->timing, t, steps);
+    if (s != RIKFAD_OK) return s;
+    *ms = t[0];
+    return RIKFAD_OK;
+}
+
+void ikfad_destroy(ikfad_ctx *ctx)
+{
+    if (!ctx) return;
+    free_tables(ctx->dev);
+    ctx->timing.release();
+    delete ctx;
+}
+
+// ------------------------------------------------------------- probes
+
+rikfad_status rikfad_probe_stream(const float *a, const float *b, const float *c, float *d,
+                                  float *e, int64_t nfloat, void *stream)
+{
+    auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
+    if (!a || !b || !c || !d || !e || nfloat < 0 || nfloat % 4 != 0)
+        return fail(RIKFAD_EINVAL, "probe_stream: NULL pointer or nfloat not a multiple of 4");
+    if (!al(a) || !al(b) || !al(c) || !al(d) || !al(e))
+        return fail(RIKFAD_EALIGN, "probe_stream: pointers must be 16-byte aligned");
+    hipError_t err = rk::launch_probe_stream(a, b, c, d, e, nfloat, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_stream");
+}
+
+rikfad_status rikfad_probe_copy(const void *src, void *dst, int64_t nbytes, void *stream)
+{
+    auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };
+    if (!src || !dst || nbytes < 0 || nbytes % 16 != 0)
+        return fail(RIKFAD_EINVAL, "probe_copy: NULL pointer or nbytes not a multiple of 16");
+    if (!al(src) || !al(dst)) return fail(RIKFAD_EALIGN, "probe_copy: pointers must be 16-byte aligned");
+    hipError_t err = rk::launch_probe_copy(src, dst, nbytes, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_copy");
+}
+
+}  // extern "C"

@@ -1,0 +1,32 @@
+// kernels.hpp -- host-side launchers of the gfx950 kernels (kernels.hip).
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include "layout.hpp"
+
+namespace rk {
+
+// Streaming pass over all tiles (matrix and vector) of a context.
+hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
+                         int64_t ntiles, float *ws, const Coeffs &k, int pending,
+                         hipStream_t stream);
+
+// Finalisation of R, C and the partial sums of R (init_only: sums only).
+hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
+                           float *ws, const Coeffs &k, int *flag, int init_only,
+                           hipStream_t stream);
+
+// Second half-kick + D over matrix tiles.
+hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, int64_t ntiles,
+                        const float *ws, const Coeffs &k, hipStream_t stream);
+
+// Full-tensor element-wise iKFAD.
+hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
+                        int64_t ntiles, const Coeffs &k, hipStream_t stream);
+
+hipError_t launch_probe_stream(const float *a, const float *b, const float *c, float *d,
+                               float *e, int64_t nfloat, hipStream_t stream);
+hipError_t launch_probe_copy(const void *s, void *d, int64_t nbytes, hipStream_t stream);
+
+}  // namespace rk

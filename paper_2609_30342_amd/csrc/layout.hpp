@@ -1,0 +1,74 @@
+// layout.hpp -- tables shared by the host planner and the gfx950 kernels.
+//
+// The step runs over a flat table of workgroup tiles covering every tensor
+// of a context (one launch for all tensors), and a table of finalisation
+// items that turn per-tile partial sums into the new friction factors.
+#pragma once
+#include <stdint.h>
+
+namespace rk {
+
+constexpr int kWave = 64;                       // CDNA wavefront
+constexpr int kWaves = 4;                       // waves per workgroup
+constexpr int kThreads = kWave * kWaves;        // 256
+constexpr int kRowsPerWave = 64;                // lane t keeps row t's partial sum
+constexpr int kStripeRows = kWaves * kRowsPerWave;  // rows per matrix tile
+constexpr int kChunkRows = kThreads;            // rows per finalisation item
+constexpr int kColItem = kWave;                 // columns per finalisation item
+constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kVecIters
+
+enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
+enum : int32_t { KIND_MATRIX = 0, KIND_VECTOR = 1 };
+enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1 };
+
+// One parameter tensor.  Offsets are in floats into the context workspace.
+struct TensorDesc {
+    void *x;           // m*n of dtype
+    float *p;          // m*n momentum
+    float *r;          // m row factor (matrix)
+    float *c;          // n column factor (matrix)
+    float *xi;         // m*n element-wise friction (vector / full iKFAD)
+    int64_t m, n;
+    int64_t rowpart;   // [ncb][m] row partial sums of [P^(1)]^2
+    int64_t colpart;   // [nrs][n] column partial sums of [P^(1)]^2
+    int64_t chunk;     // [nchunk] partial sums of R
+    int32_t nchunk, ncb, nrs, dtype;
+    int32_t kind, vec, pad0, pad1;
+};
+
+// One workgroup of the streaming pass.
+struct Tile {
+    int64_t start;     // matrix: first row; vector: first element
+    int32_t tensor;
+    int32_t count;     // matrix: rows (<= kStripeRows); vector: elements
+    int32_t col0;      // matrix: first column of the block
+    int32_t ncols;     // matrix: columns of the block (multiple of vec)
+    int32_t stripe;    // matrix: row-stripe index (row of the column partials)
+    int32_t cb;        // matrix: column-block index (row of the row partials)
+    int32_t lanes_log2;// matrix: log2 of lanes per row (rows per load = 64 >> it)
+    int32_t kind;
+    int32_t vec;       // elements per lane access: 1, 4 or 8
+    int32_t dtype;
+};
+
+// One workgroup of the finalisation pass.
+struct FinItem {
+    int32_t tensor;
+    int32_t kind;      // FIN_ROWS or FIN_COLS
+    int32_t start;     // first row / column
+    int32_t count;     // rows (<= kChunkRows) / columns (<= kColItem)
+    int32_t chunk;     // FIN_ROWS: which partial sum of R this item writes
+    int32_t pad;
+};
+
+// Step coefficients, computed in fp64 on the host and rounded once.
+struct Coeffs {
+    float h;           // step size
+    float kh;          // -(h/2) log2(e): exp(-(h/2) v) = exp2(kh v)
+    float a;           // e^{-alpha h}
+    float kappa;       // (1 - e^{-alpha h}) / (mu alpha)
+    float d;           // e^{-gamma h}
+    float eps;         // eps_stab
+};
+
+}  // namespace rk

@@ -1,0 +1,300 @@
+// plan.cpp -- validation, tile tables and workspace layout (host only).
+#include "plan.hpp"
+
+#include <cmath>
+#include <cstdint>
+
+namespace rk {
+
+namespace {
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int esize(int32_t dt) { return dt == DT_BF16 ? 2 : 4; }
+
+constexpr int64_t kMaxDim = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxElems = (int64_t(1) << 62) - 1;
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// 128-bit path when rows stay 16-byte aligned, else narrower accesses.
+int32_t matrix_vec(const rikfad_tensor &t)
+{
+    if (t.dtype == RIKFAD_FP32)
+        return (t.n % 4 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) ? 4 : 1;
+    if (t.n % 8 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) return 8;
+    if (t.n % 4 == 0 && aligned(t.x, 8) && aligned(t.g, 8) && aligned(t.p, 16)) return 4;
+    return 1;
+}
+
+int32_t flat_vec(int32_t dtype, const void *x, const void *g, const void *p, const void *xi)
+{
+    if (dtype == RIKFAD_FP32)
+        return (aligned(x, 16) && aligned(g, 16) && aligned(p, 16) && aligned(xi, 16)) ? 4 : 1;
+    if (aligned(x, 16) && aligned(g, 16) && aligned(p, 16) && aligned(xi, 16)) return 8;
+    if (aligned(x, 8) && aligned(g, 8) && aligned(p, 16) && aligned(xi, 16)) return 4;
+    return 1;
+}
+
+rikfad_status check_common(int64_t i, const void *x, const void *g, const void *p, int64_t m,
+                           int64_t n, int32_t dtype, int32_t reserved, std::string &err)
+{
+    const std::string who = "tensor " + std::to_string(i) + ": ";
+    if (reserved != 0) { err = who + "reserved field must be 0"; return RIKFAD_EINVAL; }
+    if (dtype != RIKFAD_FP32 && dtype != RIKFAD_BF16) {
+        err = who + "unsupported dtype " + std::to_string(dtype);
+        return RIKFAD_EDTYPE;
+    }
+    if (m < 1 || n < 1) { err = who + "zero-size tensor (m and n must be >= 1)"; return RIKFAD_EINVAL; }
+    if (m > kMaxDim || n > kMaxDim || m > kMaxElems / n) {
+        err = who + "too large (m, n < 2^31 and m*n < 2^62 required)";
+        return RIKFAD_EINVAL;
+    }
+    if (!x || !g || !p) { err = who + "x, g and p must be non-NULL"; return RIKFAD_EINVAL; }
+    if (!aligned(x, esize(dtype)) || !aligned(g, esize(dtype)) || !aligned(p, 4)) {
+        err = who + "pointer not aligned to its element size";
+        return RIKFAD_EALIGN;
+    }
+    return RIKFAD_OK;
+}
+
+void add_flat_tiles(Plan &pl, int32_t tensor, int64_t k, int32_t dtype, int32_t vec)
+{
+    const int64_t per = int64_t(kThreads) * vec * kVecIters;
+    for (int64_t s = 0; s < k; s += per) {
+        Tile t{};
+        t.start = s;
+        t.tensor = tensor;
+        t.count = static_cast<int32_t>(k - s < per ? k - s : per);
+        t.kind = KIND_VECTOR;
+        t.vec = vec;
+        t.dtype = dtype;
+        pl.tiles.push_back(t);
+    }
+}
+
+}  // namespace
+
+rikfad_status check_hparams(const rikfad_hparams *hp, std::string &err)
+{
+    if (!hp) { err = "hparams is NULL"; return RIKFAD_EINVAL; }
+    if (!(std::isfinite(hp->h) && std::isfinite(hp->gamma) && std::isfinite(hp->alpha) &&
+          std::isfinite(hp->mu) && std::isfinite(hp->eps_stab))) {
+        err = "hyperparameters must be finite";
+        return RIKFAD_EINVAL;
+    }
+    if (!(hp->h > 0) || !(hp->mu > 0) || hp->alpha < 0 || hp->gamma < 0 || hp->eps_stab < 0) {
+        err = "need h > 0, mu > 0, alpha >= 0, gamma >= 0, eps_stab >= 0";
+        return RIKFAD_EINVAL;
+    }
+    const Coeffs k = make_coeffs(*hp);
+    if (!(std::isfinite(k.h) && std::isfinite(k.kh) && std::isfinite(k.kappa) &&
+          std::isfinite(k.eps))) {
+        err = "hyperparameters give step coefficients outside the fp32 range";
+        return RIKFAD_EINVAL;
+    }
+    return RIKFAD_OK;
+}
+
+// App. A Table rows C and D: e^{-alpha h}, (1 - e^{-alpha h})/(mu alpha)
+// evaluated as -expm1(-alpha h)/(mu alpha) (alpha = 0: its limit h/mu),
+// e^{-gamma h}; and -(h/2) log2(e) so that the half-kick is one exp2.
+// All in fp64, rounded once to fp32.
+Coeffs make_coeffs(const rikfad_hparams &hp)
+{
+    const double ah = hp.alpha * hp.h;
+    Coeffs k;
+    k.h = static_cast<float>(hp.h);
+    k.kh = static_cast<float>(-0.5 * hp.h * 1.44269504088896340736);
+    k.a = static_cast<float>(std::exp(-ah));
+    k.kappa = static_cast<float>(hp.alpha > 0 ? -std::expm1(-ah) / (hp.mu * hp.alpha)
+                                              : hp.h / hp.mu);
+    k.d = static_cast<float>(std::exp(-hp.gamma * hp.h));
+    k.eps = static_cast<float>(hp.eps_stab);
+    return k;
+}
+
+bool grad_fits(const void *g, int32_t dtype, int32_t vec)
+{
+    if (!g) return false;
+    return aligned(g, static_cast<uintptr_t>(esize(dtype)) * static_cast<uintptr_t>(vec));
+}
+
+rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::string &err)
+{
+    if (count < 0 || (count > 0 && !t)) {
+        err = "tensor list is NULL or count < 0";
+        return RIKFAD_EINVAL;
+    }
+    pl = Plan{};
+    for (int64_t i = 0; i < count; ++i) {
+        const rikfad_tensor &T = t[i];
+        rikfad_status s = check_common(i, T.x, T.g, T.p, T.m, T.n, T.dtype, T.reserved, err);
+        if (s != RIKFAD_OK) return s;
+        const bool vec = (T.m == 1 || T.n == 1);
+        float *xi = (T.m == 1) ? T.c : T.r;
+        if (vec ? !xi : (!T.r || !T.c)) {
+            err = "tensor " + std::to_string(i) +
+                  (vec ? ": vector friction (c when m == 1, else r) is NULL"
+                       : ": factors r and c must be non-NULL");
+            return RIKFAD_EINVAL;
+        }
+        if ((T.r && !aligned(T.r, 4)) || (T.c && !aligned(T.c, 4))) {
+            err = "tensor " + std::to_string(i) + ": factor pointer not 4-byte aligned";
+            return RIKFAD_EALIGN;
+        }
+    }
+
+    int64_t ws = 0;
+    pl.tensors.resize(static_cast<size_t>(count));
+    pl.grads.resize(static_cast<size_t>(count));
+    std::vector<Tile> vec_tiles;
+    std::vector<FinItem> col_items;
+    for (int64_t i = 0; i < count; ++i) {
+        const rikfad_tensor &T = t[i];
+        TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
+        d = TensorDesc{};
+        d.x = T.x;
+        d.p = T.p;
+        d.r = T.r;
+        d.c = T.c;
+        d.m = T.m;
+        d.n = T.n;
+        d.dtype = T.dtype;
+        pl.grads[static_cast<size_t>(i)] = T.g;
+        const int64_t mn = T.m * T.n;
+        const int64_t eb = esize(T.dtype);
+        pl.elements += mn;
+        pl.ikfad_state_bytes += 8 * mn;
+        if (T.m == 1 || T.n == 1) {
+            d.kind = KIND_VECTOR;
+            d.xi = (T.m == 1) ? T.c : T.r;
+            d.vec = flat_vec(T.dtype, T.x, T.g, T.p, d.xi);
+            pl.vectors += 1;
+            pl.state_bytes += 8 * mn;
+            pl.min_bytes += mn * (3 * eb + 16);        // read x g p xi, write x p xi
+            pl.stream_min_bytes += mn * (3 * eb + 16);
+            Plan tmp;
+            add_flat_tiles(tmp, static_cast<int32_t>(i), mn, T.dtype, d.vec);
+            vec_tiles.insert(vec_tiles.end(), tmp.tiles.begin(), tmp.tiles.end());
+            continue;
+        }
+        d.kind = KIND_MATRIX;
+        d.vec = matrix_vec(T);
+        pl.matrices += 1;
+        pl.state_bytes += 4 * mn + 4 * (T.m + T.n);
+        pl.min_bytes += mn * (3 * eb + 8) + 8 * (T.m + T.n);   // x g p in, x p out; R C
+        pl.stream_min_bytes += mn * (3 * eb + 8) + 4 * (T.m + T.n); // R, C read only
+
+        // Column blocks of up to 64 lanes x vec columns; a narrow last block
+        // uses the smallest power-of-two lane count that covers it.
+        struct Block { int32_t col0, ncols, llog; };
+        std::vector<Block> blocks;
+        const int64_t lanes = T.n / d.vec;
+        const int64_t full = lanes / kWave, rem = lanes % kWave;
+        for (int64_t b = 0; b < full; ++b)
+            blocks.push_back({static_cast<int32_t>(b * kWave * d.vec), kWave * d.vec, 6});
+        if (rem > 0) {
+            int llog = 0;
+            while ((int64_t(1) << llog) < rem) ++llog;
+            blocks.push_back({static_cast<int32_t>(full * kWave * d.vec),
+                              static_cast<int32_t>(rem * d.vec), llog});
+        }
+        d.ncb = static_cast<int32_t>(blocks.size());
+        d.nrs = static_cast<int32_t>(ceil_div(T.m, kStripeRows));
+        d.nchunk = static_cast<int32_t>(ceil_div(T.m, kChunkRows));
+        d.rowpart = ws;
+        ws += round_up(T.m * d.ncb, 64);
+        d.colpart = ws;
+        ws += round_up(int64_t(d.nrs) * T.n, 64);
+        d.chunk = ws;
+        ws += round_up(d.nchunk, 64);
+
+        for (int32_t s = 0; s < d.nrs; ++s) {
+            for (int32_t b = 0; b < d.ncb; ++b) {
+                Tile tl{};
+                tl.start = int64_t(s) * kStripeRows;
+                tl.tensor = static_cast<int32_t>(i);
+                tl.count = static_cast<int32_t>(
+                    T.m - tl.start < kStripeRows ? T.m - tl.start : kStripeRows);
+                tl.col0 = blocks[static_cast<size_t>(b)].col0;
+                tl.ncols = blocks[static_cast<size_t>(b)].ncols;
+                tl.stripe = s;
+                tl.cb = b;
+                tl.lanes_log2 = blocks[static_cast<size_t>(b)].llog;
+                tl.kind = KIND_MATRIX;
+                tl.vec = d.vec;
+                tl.dtype = T.dtype;
+                pl.tiles.push_back(tl);
+            }
+        }
+        for (int32_t q = 0; q < d.nchunk; ++q) {
+            const int64_t r0 = int64_t(q) * kChunkRows;
+            pl.fin.push_back({static_cast<int32_t>(i), FIN_ROWS, static_cast<int32_t>(r0),
+                              static_cast<int32_t>(T.m - r0 < kChunkRows ? T.m - r0 : kChunkRows),
+                              q, 0});
+        }
+        for (int64_t j0 = 0; j0 < T.n; j0 += kColItem)
+            col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
+                                 static_cast<int32_t>(T.n - j0 < kColItem ? T.n - j0 : kColItem),
+                                 0, 0});
+    }
+    pl.matrix_tiles = static_cast<int64_t>(pl.tiles.size());
+    pl.tiles.insert(pl.tiles.end(), vec_tiles.begin(), vec_tiles.end());
+    pl.row_items = static_cast<int64_t>(pl.fin.size());
+    pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());
+    pl.ws_floats = ws;
+    if (pl.tiles.size() > static_cast<size_t>(INT32_MAX) || pl.fin.size() > static_cast<size_t>(INT32_MAX)) {
+        err = "parameter set needs more than 2^31 workgroups";
+        return RIKFAD_EINVAL;
+    }
+    return RIKFAD_OK;
+}
+
+rikfad_status plan_ikfad(const ikfad_tensor *t, int64_t count, Plan &pl, std::string &err)
+{
+    if (count < 0 || (count > 0 && !t)) {
+        err = "tensor list is NULL or count < 0";
+        return RIKFAD_EINVAL;
+    }
+    pl = Plan{};
+    pl.tensors.resize(static_cast<size_t>(count));
+    pl.grads.resize(static_cast<size_t>(count));
+    for (int64_t i = 0; i < count; ++i) {
+        const ikfad_tensor &T = t[i];
+        rikfad_status s = check_common(i, T.x, T.g, T.p, T.m, T.n, T.dtype, T.reserved, err);
+        if (s != RIKFAD_OK) return s;
+        if (!T.xi) { err = "tensor " + std::to_string(i) + ": xi is NULL"; return RIKFAD_EINVAL; }
+        if (!aligned(T.xi, 4)) {
+            err = "tensor " + std::to_string(i) + ": xi not 4-byte aligned";
+            return RIKFAD_EALIGN;
+        }
+        TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
+        d = TensorDesc{};
+        d.x = T.x;
+        d.p = T.p;
+        d.xi = T.xi;
+        d.m = T.m;
+        d.n = T.n;
+        d.dtype = T.dtype;
+        d.kind = KIND_VECTOR;
+        d.vec = flat_vec(T.dtype, T.x, T.g, T.p, T.xi);
+        pl.grads[static_cast<size_t>(i)] = T.g;
+        const int64_t mn = T.m * T.n;
+        pl.elements += mn;
+        pl.vectors += 1;
+        pl.state_bytes += 8 * mn;
+        pl.ikfad_state_bytes += 8 * mn;
+        pl.min_bytes += mn * (3 * esize(T.dtype) + 16);
+        pl.stream_min_bytes += mn * (3 * esize(T.dtype) + 16);
+        add_flat_tiles(pl, static_cast<int32_t>(i), mn, T.dtype, d.vec);
+    }
+    if (pl.tiles.size() > static_cast<size_t>(INT32_MAX)) {
+        err = "parameter set needs more than 2^31 workgroups";
+        return RIKFAD_EINVAL;
+    }
+    return RIKFAD_OK;
+}
+
+}  // namespace rk

@@ -1,0 +1,194 @@
+"""Shared machinery of the GPU parity tests: run the HIP path (through the C
+ABI binding) and the fp64 oracle on the same seeded inputs and compare.
+
+Error metric (per tensor and quantity): max_i |a_i - b_i| / max(|b_i|, rms(b))
+for x and p, where the rms floor keeps a near-cancellation in P^(B) from
+dominating; plain max relative error for the factors R, C (non-negative,
+no cancellation; 0/0 counts as 0).  Tolerances: 1e-5 for fp32 state; for a
+bf16 parameter the stored value is compared with the oracle's unrounded
+fp64 update from the same bf16 starting point, which bf16 rounding keeps
+within half an ulp (<= 2^-8 relative) -- 4e-3 with the rms floor.
+"""
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+import oracle as O
+from paper_2609_30342_amd import rikfad as R
+from paper_2609_30342_amd import synth
+
+TOL_F32 = 1e-5
+TOL_BF16 = 4e-3
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def rel_rms(got, want):
+    got = np.asarray(got, dtype=np.float64).reshape(want.shape)
+    if want.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(got)):
+        return float("inf")
+    floor = np.sqrt(np.mean(want * want))
+    den = np.maximum(np.abs(want), floor)
+    den = np.where(den == 0, 1.0, den)
+    return float(np.max(np.abs(got - want) / den))
+
+
+def rel_plain(got, want):
+    got = np.asarray(got, dtype=np.float64).reshape(want.shape)
+    if want.size == 0:
+        return 0.0
+    if not np.all(np.isfinite(got)):
+        return float("inf")
+    diff = np.abs(got - want)
+    den = np.abs(want)
+    out = np.where(den > 0, diff / np.where(den > 0, den, 1.0), np.where(diff > 0, np.inf, 0.0))
+    return float(np.max(out))
+
+
+def host(t):
+    return t.detach().to(torch.float64).cpu().numpy()
+
+
+@dataclass
+class Pair:
+    """GPU context + oracle state over one parameter list."""
+    specs: list
+    wl: synth.Workload
+    xs: list
+    gs: list
+    opt: R.RIKFAD
+    ref: list
+    checked: list        # indices the oracle follows
+
+
+def make_pair(specs, hp, seed=0, scales="lognormal", two_pass=False, checked=None,
+              device="cuda:0", x_offset=0):
+    """x_offset > 0 places each parameter and gradient that many elements into
+    a larger buffer (misaligned views, scalar path)."""
+    wl = synth.Workload(specs, seed=seed, scales=scales)
+    checked = list(range(len(specs))) if checked is None else list(checked)
+    xs, gs = [], []
+    for i, sp in enumerate(specs):
+        dt = torch.bfloat16 if sp.dtype == "bf16" else torch.float32
+        if i in checked or sp.numel < 1 << 22:
+            x0 = torch.from_numpy(wl.x0(i)).to(dt)
+        else:
+            gen = torch.Generator(device=device).manual_seed(seed * 1000 + i)
+            x0 = (torch.randn((sp.m, sp.n), generator=gen, device=device) * 0.02).to(dt)
+        if x_offset:
+            xb = torch.empty(sp.numel + x_offset, dtype=dt, device=device)
+            gb = torch.empty(sp.numel + x_offset, dtype=dt, device=device)
+            x = xb[x_offset:].view(sp.m, sp.n)
+            g = gb[x_offset:].view(sp.m, sp.n)
+            x.copy_(x0)
+        else:
+            x = x0.to(device).contiguous()
+            g = torch.empty_like(x)
+        xs.append(x)
+        gs.append(g)
+    opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
+    ref = {i: O.make_tensor(wl.x0(i).astype(np.float64), bf16=(specs[i].dtype == "bf16"),
+                            track_unrounded=(specs[i].dtype == "bf16"))
+           for i in checked}
+    return Pair(specs, wl, xs, gs, opt, ref, checked)
+
+
+def load_grads(pair, step, seed_unchecked=0):
+    """Write step `step`'s gradients into the GPU buffers; returns the host
+    copies of the checked tensors' gradients (same bits)."""
+    host_g = {}
+    for i, sp in enumerate(pair.specs):
+        if i in pair.ref or sp.numel < 1 << 22:
+            g = pair.wl.grad(i, step)
+            if i in pair.ref:
+                host_g[i] = g
+            pair.gs[i].copy_(torch.from_numpy(g).to(pair.gs[i].dtype).view_as(pair.gs[i]))
+        else:
+            gen = torch.Generator(device=pair.gs[i].device).manual_seed(
+                (seed_unchecked + 1) * 7919 + step * 131 + i)
+            pair.gs[i].copy_(torch.randn(pair.gs[i].shape, generator=gen,
+                                         device=pair.gs[i].device).to(pair.gs[i].dtype))
+    return host_g
+
+
+def oracle_step(pair, host_g, hp, threads=16):
+    idx = sorted(pair.ref)
+    O.step_list([pair.ref[i] for i in idx], [host_g[i] for i in idx], O.HParams(**hp),
+                threads=threads)
+
+
+def compare(pair, sync=True, what=("x", "p", "r", "c")):
+    """Max error per quantity over the checked tensors (fp32 tensors and
+    bf16 tensors separately for x)."""
+    if sync:
+        pair.opt.sync_momentum()
+    torch.cuda.synchronize()
+    errs = {"x": 0.0, "x_bf16": 0.0, "p": 0.0, "r": 0.0, "c": 0.0}
+    for i, o in pair.ref.items():
+        p, r, c = pair.opt.state[i]
+        if "x" in what:
+            if o.bf16:
+                errs["x_bf16"] = max(errs["x_bf16"], rel_rms(host(pair.xs[i]), o.x_unrounded))
+            else:
+                errs["x"] = max(errs["x"], rel_rms(host(pair.xs[i]), o.x))
+        if "p" in what:
+            errs["p"] = max(errs["p"], rel_rms(host(p), o.p))
+        if o.is_vector:
+            xi = c if o.m == 1 else r
+            if "r" in what:
+                errs["r"] = max(errs["r"], rel_plain(host(xi), o.xi))
+        else:
+            if "r" in what:
+                errs["r"] = max(errs["r"], rel_plain(host(r), o.r))
+            if "c" in what:
+                errs["c"] = max(errs["c"], rel_plain(host(c), o.c))
+    return errs
+
+
+def reset_bf16_x(pair):
+    """Give the GPU the oracle's current bf16 parameters (exact values), so a
+    step's bf16 result can be compared with the oracle's unrounded update
+    from the same starting point."""
+    for i, o in pair.ref.items():
+        if o.bf16:
+            pair.xs[i].copy_(torch.from_numpy(o.x).to(torch.bfloat16).view_as(pair.xs[i]))
+
+
+def assert_ok(errs, tol=TOL_F32, tol_bf16=TOL_BF16, label=""):
+    bad = {k: v for k, v in errs.items()
+           if (v > tol_bf16 if k == "x_bf16" else v > tol)}
+    assert not bad, f"{label}: errors over tolerance {bad} (all: {errs})"
+
+
+def run_parity(specs, hp, steps, seed=0, scales="lognormal", two_pass=False, checked=None,
+               label="", sync_every=None, x_offset=0, threads=16):
+    pair = make_pair(specs, hp, seed=seed, scales=scales, two_pass=two_pass, checked=checked,
+                     x_offset=x_offset)
+    has_bf16 = any(pair.ref[i].bf16 for i in pair.ref)
+    worst = {}
+    for s in range(steps):
+        if steps <= 5 or s % 10 == 0:
+            log(f"[parity] {label} step {s}")
+        if has_bf16:
+            reset_bf16_x(pair)
+        hg = load_grads(pair, s, seed)
+        pair.opt.step()
+        oracle_step(pair, hg, hp, threads=threads)
+        if has_bf16:
+            e = compare(pair, sync=False, what=("x",))
+            worst["x_bf16"] = max(worst.get("x_bf16", 0.0), e["x_bf16"])
+        if sync_every and (s + 1) % sync_every == 0:
+            pair.opt.sync_momentum()
+    errs = compare(pair)
+    if has_bf16:
+        errs["x_bf16"] = max(errs["x_bf16"], worst["x_bf16"])
+    log(f"[parity] {label} steps={steps} errs={ {k: f'{v:.2e}' for k, v in errs.items()} }")
+    return pair, errs
