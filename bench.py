@@ -75,8 +75,7 @@ def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0):
     info = opt.query()
     for _ in range(warmup):
         opt.step()
-    torch.cuda.synchronize()
-    R.rikfad_timing_enable(opt.ctx, True)
+    # Timed region: exactly `steps` steps, no per-kernel events.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -85,6 +84,11 @@ def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0):
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end)
+    # Kernel breakdown: the same number of steps again with the library's
+    # HIP events around each launch (on the step's stream).
+    R.rikfad_timing_enable(opt.ctx, True)
+    for _ in range(steps):
+        opt.step()
     k1, k2, k3, n = R.rikfad_timing_read(opt.ctx)
     R.rikfad_timing_enable(opt.ctx, False)
     nonfinite = opt.nonfinite()
@@ -176,10 +180,13 @@ def main():
                     help="seconds of oracle time for cpu_baseline (0 = skip)")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the bf16 / two-pass / full-iKFAD / probe side measurements")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run the copy probe 3 times over this many MiB (a kernel of "
+                         "known traffic for scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding is described in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
+              "supported", file=sys.stderr)
         return 2
 
     import torch
@@ -253,6 +260,17 @@ def main():
                                       "state_bytes": info["ikfad_state_bytes"]}
         var["probe_3r2w_gbps"] = time_probe(N)
         out["variants"] = var
+    if args.calibrate_copy_mib > 0:
+        nbytes = args.calibrate_copy_mib << 20
+        src = torch.ones(nbytes // 4, device="cuda:0")
+        dst = torch.empty_like(src)
+        from paper_2609_30342_amd import rikfad as R
+        for _ in range(3):
+            R.rikfad_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes,
+                                torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = nbytes
+        del src, dst
     if args.cpu_budget > 0:
         out["cpu_baseline"] = cpu_baseline(specs, hp, args.cpu_budget)
     else:

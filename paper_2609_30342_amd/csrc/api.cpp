@@ -241,8 +241,9 @@ rikfad_status rikfad_create(const rikfad_tensor *tensors, int64_t count,
 static rikfad_status apply_pending(rikfad_ctx *ctx, hipStream_t stream)
 {
     if (!ctx->pending) return RIKFAD_OK;
-    hipError_t e = rk::launch_apply(ctx->dev.tensors, ctx->dev.tiles, ctx->plan.matrix_tiles,
-                                    ctx->dev.ws, ctx->k, stream);
+    hipError_t e = rk::launch_apply(ctx->dev.tensors, ctx->dev.tiles, ctx->plan.groups.data(),
+                                    static_cast<int>(ctx->plan.groups.size()), ctx->dev.ws,
+                                    ctx->k, stream);
     if (e != hipSuccess) return hip_fail(e, "launch apply kernel");
     ctx->pending = false;
     return RIKFAD_OK;
@@ -264,8 +265,8 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     Timing &tm = ctx->timing;
     rikfad_status s;
     if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
-    e = rk::launch_stream(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
-                          static_cast<int64_t>(pl.tiles.size()), ctx->dev.ws, ctx->k,
+    e = rk::launch_stream(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles, pl.groups.data(),
+                          static_cast<int>(pl.groups.size()), ctx->dev.ws, ctx->k,
                           ctx->pending ? 1 : 0, stream);
     if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
     ctx->pending = false;

@@ -44,6 +44,33 @@ __device__ __forceinline__ RK_GLOBAL T *gmem(T *q)
     return (RK_GLOBAL T *)q;
 }
 
+// Streams are read and written exactly once per step.  With RK_NT the
+// accesses carry the non-temporal hint so they do not displace the small,
+// reused data (factors, partial sums, tables) from the caches.
+#ifndef RK_NT
+#define RK_NT 1
+#endif
+
+template <typename T>
+__device__ __forceinline__ T ldg(const T *q)
+{
+#if RK_NT
+    return __builtin_nontemporal_load(gmem(q));
+#else
+    return *gmem(q);
+#endif
+}
+
+template <typename T>
+__device__ __forceinline__ void stg(T *q, T v)
+{
+#if RK_NT
+    __builtin_nontemporal_store(v, gmem(q));
+#else
+    *gmem(q) = v;
+#endif
+}
+
 // Native clang vectors (the HIP float4 class cannot bind to an
 // address-space-qualified reference).
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -74,39 +101,39 @@ template <typename T, int V> struct Io;
 template <> struct Io<float, 4> {
     static __device__ __forceinline__ void load(const float *q, float (&o)[4])
     {
-        const f32x4 v = *gmem(reinterpret_cast<const f32x4 *>(q));
+        const f32x4 v = ldg(reinterpret_cast<const f32x4 *>(q));
         o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
     }
     static __device__ __forceinline__ void store(float *q, const float (&o)[4])
     {
-        *gmem(reinterpret_cast<f32x4 *>(q)) = f32x4{o[0], o[1], o[2], o[3]};
+        stg(reinterpret_cast<f32x4 *>(q), f32x4{o[0], o[1], o[2], o[3]});
     }
 };
 
 template <> struct Io<float, 8> {
     static __device__ __forceinline__ void load(const float *q, float (&o)[8])
     {
-        const f32x4 a = gmem(reinterpret_cast<const f32x4 *>(q))[0];
-        const f32x4 b = gmem(reinterpret_cast<const f32x4 *>(q))[1];
+        const f32x4 a = ldg(reinterpret_cast<const f32x4 *>(q));
+        const f32x4 b = ldg(reinterpret_cast<const f32x4 *>(q) + 1);
         o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
         o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
     }
     static __device__ __forceinline__ void store(float *q, const float (&o)[8])
     {
-        gmem(reinterpret_cast<f32x4 *>(q))[0] = f32x4{o[0], o[1], o[2], o[3]};
-        gmem(reinterpret_cast<f32x4 *>(q))[1] = f32x4{o[4], o[5], o[6], o[7]};
+        stg(reinterpret_cast<f32x4 *>(q), f32x4{o[0], o[1], o[2], o[3]});
+        stg(reinterpret_cast<f32x4 *>(q) + 1, f32x4{o[4], o[5], o[6], o[7]});
     }
 };
 
 template <> struct Io<float, 1> {
-    static __device__ __forceinline__ void load(const float *q, float (&o)[1]) { o[0] = *gmem(q); }
-    static __device__ __forceinline__ void store(float *q, const float (&o)[1]) { *gmem(q) = o[0]; }
+    static __device__ __forceinline__ void load(const float *q, float (&o)[1]) { o[0] = ldg(q); }
+    static __device__ __forceinline__ void store(float *q, const float (&o)[1]) { stg(q, o[0]); }
 };
 
 template <> struct Io<uint16_t, 8> {
     static __device__ __forceinline__ void load(const uint16_t *q, float (&o)[8])
     {
-        const u32x4 v = *gmem(reinterpret_cast<const u32x4 *>(q));
+        const u32x4 v = ldg(reinterpret_cast<const u32x4 *>(q));
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -121,14 +148,14 @@ template <> struct Io<uint16_t, 8> {
         for (int i = 0; i < 4; ++i)
             w[i] = static_cast<uint32_t>(f32_to_bf16(o[2 * i])) |
                    (static_cast<uint32_t>(f32_to_bf16(o[2 * i + 1])) << 16);
-        *gmem(reinterpret_cast<u32x4 *>(q)) = u32x4{w[0], w[1], w[2], w[3]};
+        stg(reinterpret_cast<u32x4 *>(q), u32x4{w[0], w[1], w[2], w[3]});
     }
 };
 
 template <> struct Io<uint16_t, 4> {
     static __device__ __forceinline__ void load(const uint16_t *q, float (&o)[4])
     {
-        const u32x2 v = *gmem(reinterpret_cast<const u32x2 *>(q));
+        const u32x2 v = ldg(reinterpret_cast<const u32x2 *>(q));
         o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
         o[2] = __uint_as_float(v.y << 16); o[3] = __uint_as_float(v.y & 0xffff0000u);
     }
@@ -138,13 +165,13 @@ template <> struct Io<uint16_t, 4> {
                            (static_cast<uint32_t>(f32_to_bf16(o[1])) << 16);
         const uint32_t b = static_cast<uint32_t>(f32_to_bf16(o[2])) |
                            (static_cast<uint32_t>(f32_to_bf16(o[3])) << 16);
-        *gmem(reinterpret_cast<u32x2 *>(q)) = u32x2{a, b};
+        stg(reinterpret_cast<u32x2 *>(q), u32x2{a, b});
     }
 };
 
 template <> struct Io<uint16_t, 1> {
-    static __device__ __forceinline__ void load(const uint16_t *q, float (&o)[1]) { o[0] = bf16_to_f32(*gmem(q)); }
-    static __device__ __forceinline__ void store(uint16_t *q, const float (&o)[1]) { *gmem(q) = f32_to_bf16(o[0]); }
+    static __device__ __forceinline__ void load(const uint16_t *q, float (&o)[1]) { o[0] = bf16_to_f32(ldg(q)); }
+    static __device__ __forceinline__ void store(uint16_t *q, const float (&o)[1]) { stg(q, f32_to_bf16(o[0])); }
 };
 
 // ---------------------------------------------------------- reductions
@@ -171,12 +198,26 @@ __device__ __forceinline__ float row_rate(float kh, float r_i, float denom)
 
 // ------------------------------------------------ streaming pass (matrix)
 //
-// A tile is kStripeRows rows x one column block.  Each wave walks
-// kRowsPerWave consecutive rows; a row of the block is covered by L lanes
+// A tile is 4 x rpw rows x one column block.  Each wave walks rpw
+// consecutive rows; a row of the block is covered by L lanes
 // (L = 64 for wide blocks; narrow blocks put 64/L rows in one load), each
 // lane owning V consecutive columns.  Column sums accumulate in the lane's
 // registers while it walks down the rows; row sums are reduced across the
 // L lanes of a row with xor shuffles and parked in lane (row - first row).
+
+// Loads row rl of a wave's rows into one ring slot.  Outside the tile the
+// lane reads the wave's first row instead (always in bounds when the wave
+// has rows) and the caller masks the result, so the load is unconditional.
+template <typename XT, int V>
+__device__ __forceinline__ void load_row(const XT *x, const XT *g, const float *p, int64_t r0,
+                                         int64_t n, int64_t col, bool ok, int rl,
+                                         float (&xs)[V], float (&gs)[V], float (&qs)[V])
+{
+    const int64_t off = ok ? (r0 + rl) * n + col : r0 * n + col;
+    Io<XT, V>::load(x + off, xs);
+    Io<XT, V>::load(g + off, gs);
+    Io<float, V>::load(p + off, qs);
+}
 
 template <typename XT, int V>
 __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
@@ -194,62 +235,75 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     const int ccol = sl * V;
     const bool colok = ccol < tile.ncols;
     const int64_t col = tile.col0 + ccol;
+    const int64_t r0 = tile.start + static_cast<int64_t>(wave) * tile.rpw;
+    const int nr = max(0, min(tile.rpw, static_cast<int>(tile.start + tile.count - r0)));
+    const int nld = (nr + G - 1) >> (6 - llog);   // row loads of this wave
+    XT *__restrict__ x = static_cast<XT *>(td.x);
+    float *__restrict__ p = td.p;
+
+    // Ring of kBatch row loads: the load of row-load ld + kBatch is issued
+    // as soon as row-load ld has been consumed, so every wave keeps kBatch
+    // 1 KB requests per stream in flight.  The first loads go out before
+    // the factor sum is read, hiding its latency.
+    float xv[kBatch][V], gv[kBatch][V], qv[kBatch][V];
+    // A lane outside the block's columns reads the block's first column.
+    const int64_t lcol = colok ? col : tile.col0;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+        if (nr > 0)
+            load_row<XT, V>(x, g, p, r0, n, lcol, colok && u * G + seg < nr, u * G + seg, xv[u],
+                            gv[u], qv[u]);
 
     float cv[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) cv[i] = colok ? gmem(td.c)[col + i] : 0.f;
-
     const float denom = sum_r(ws + td.chunk, td.nchunk) + k.eps;
-    const int64_t r0 = tile.start + static_cast<int64_t>(wave) * kRowsPerWave;
-    const int nr = max(0, min(kRowsPerWave, static_cast<int>(tile.start + tile.count - r0)));
     const float myrate = lane < nr ? row_rate(k.kh, gmem(td.r)[r0 + lane], denom) : 0.f;
 
-    XT *__restrict__ x = static_cast<XT *>(td.x);
-    float *__restrict__ p = td.p;
     float acc[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
     float myrow = 0.f;
 
-    const int nld = (nr + G - 1) >> (6 - llog);
-    for (int ld = 0; ld < nld; ++ld) {
-        const int rl = ld * G + seg;
-        const bool ok = colok && rl < nr;
-        const float rate = __shfl(myrate, rl & (kWave - 1));
-        const int64_t off = (r0 + rl) * n + col;
-        float xv[V], gv[V], qv[V];
-        if (ok) {
-            Io<XT, V>::load(x + off, xv);
-            Io<XT, V>::load(g + off, gv);
-            Io<float, V>::load(p + off, qv);
-        } else {
+    for (int ld0 = 0; ld0 < nld; ld0 += kBatch) {
 #pragma unroll
-            for (int i = 0; i < V; ++i) xv[i] = gv[i] = qv[i] = 0.f;
-        }
-        float rs = 0.f;
+        for (int u = 0; u < kBatch; ++u) {
+            const int ld = ld0 + u;
+            const int rl = ld * G + seg;
+            const bool ok = colok && rl < nr;
+            const float rate = __shfl(myrate, rl & (kWave - 1));
+            float rs = 0.f;
 #pragma unroll
-        for (int i = 0; i < V; ++i) {
-            const float e = exp2f(rate * cv[i]);
-            const float pn = pending ? k.d * (qv[i] * e) : qv[i];
-            const float pb = pn - k.h * gv[i];
-            xv[i] = xv[i] + k.h * pb;
-            const float p1 = pb * e;
-            qv[i] = p1;
-            const float s = ok ? p1 * p1 : 0.f;
-            acc[i] += s;
-            rs += s;
+            for (int i = 0; i < V; ++i) {
+                const float q = ok ? qv[u][i] : 0.f;
+                const float gg = ok ? gv[u][i] : 0.f;
+                const float e = exp2f(rate * cv[i]);
+                const float pn = pending ? k.d * (q * e) : q;
+                const float pb = pn - k.h * gg;
+                xv[u][i] = xv[u][i] + k.h * pb;
+                const float p1 = pb * e;
+                qv[u][i] = p1;
+                const float sq = ok ? p1 * p1 : 0.f;
+                acc[i] += sq;
+                rs += sq;
+            }
+            if (ok) {
+                const int64_t off = (r0 + rl) * n + col;
+                Io<XT, V>::store(x + off, xv[u]);
+                Io<float, V>::store(p + off, qv[u]);
+            }
+            const int rn = (ld + kBatch) * G + seg;
+            if (ld + kBatch < nld)
+                load_row<XT, V>(x, g, p, r0, n, lcol, colok && rn < nr, rn, xv[u], gv[u], qv[u]);
+            for (int o = 1; o < L; o <<= 1) rs += __shfl_xor(rs, o);
+            const int first = ld * G;                 // first row of this load
+            const float v = __shfl(rs, ((lane - first) & (G - 1)) << llog);
+            if (lane >= first && lane < first + G) myrow = v;
         }
-        if (ok) {
-            Io<XT, V>::store(x + off, xv);
-            Io<float, V>::store(p + off, qv);
-        }
-        for (int o = 1; o < L; o <<= 1) rs += __shfl_xor(rs, o);
-        const float v = __shfl(rs, ((lane - ld * G) & (G - 1)) << llog);
-        if (lane >= ld * G && lane < ld * G + G) myrow = v;
     }
 
     // Lanes l and l ^ o (o >= L) own the same columns: fold them, then fold
-    // the four waves through LDS in wave order.
+    // the waves through LDS in wave order.
     for (int o = L; o < kWave; o <<= 1) {
 #pragma unroll
         for (int i = 0; i < V; ++i) acc[i] += __shfl_xor(acc[i], o);
@@ -260,10 +314,11 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     }
     __syncthreads();
     float *colpart = ws + td.colpart + static_cast<int64_t>(tile.stripe) * n + tile.col0;
-    for (int j = threadIdx.x; j < tile.ncols; j += kThreads) {
-        const float s = ((lds[j] + lds[kWave * V + j]) + lds[2 * kWave * V + j]) +
-                        lds[3 * kWave * V + j];
-        gmem(colpart)[j] = s;
+    for (int j = threadIdx.x; j < tile.ncols; j += kStreamThreads) {
+        float sum = lds[j];
+#pragma unroll
+        for (int w = 1; w < kStreamWaves; ++w) sum += lds[w * kWave * V + j];
+        gmem(colpart)[j] = sum;
     }
     if (lane < nr) gmem(ws)[td.rowpart + static_cast<int64_t>(tile.cb) * td.m + r0 + lane] = myrow;
 }
@@ -296,67 +351,63 @@ __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__rest
     Io<float, V>::store(xi, fv);
 }
 
-template <typename XT, int V>
+template <typename XT, int V, int NTH>
 __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
                                   float *__restrict__ p, float *__restrict__ xi,
                                   int64_t start, int count, const Coeffs &k)
 {
     const int full = count - count % V;
-    for (int e = threadIdx.x * V; e < full; e += kThreads * V) {
+    for (int e = threadIdx.x * V; e < full; e += NTH * V) {
         const int64_t o = start + e;
         ikfad_elems<XT, V>(x + o, g + o, p + o, xi + o, k);
     }
-    for (int e = full + threadIdx.x; e < count; e += kThreads) {
+    for (int e = full + threadIdx.x; e < count; e += NTH) {
         const int64_t o = start + e;
         ikfad_elems<XT, 1>(x + o, g + o, p + o, xi + o, k);
     }
 }
 
-template <typename XT>
+template <typename XT, int NTH>
 __device__ void elementwise_tile(const TensorDesc &td, const void *g, const Tile &tile,
                                  const Coeffs &k)
 {
     XT *x = static_cast<XT *>(td.x);
     const XT *gg = static_cast<const XT *>(g);
     if (tile.vec == 8)
-        elementwise_range<XT, 8>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 8, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
     else if (tile.vec == 4)
-        elementwise_range<XT, 4>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 4, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
     else
-        elementwise_range<XT, 1>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 1, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
 }
 
 // ------------------------------------------------------------- kernels
 
-__global__ __launch_bounds__(kThreads) void rikfad_stream_kernel(
+// One instantiation per (storage type, access width) of the matrix tiles it
+// serves, so each carries only the registers its own path needs; vector
+// tiles of the same storage type ride along (element-wise iKFAD).
+template <typename XT, int V>
+__global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
-    const Tile *__restrict__ tiles, float *__restrict__ ws, Coeffs k, int pending)
+    const Tile *__restrict__ tiles, int64_t tile0, float *__restrict__ ws, Coeffs k,
+    int pending)
 {
-    __shared__ float lds[kWaves * kWave * 8];
-    const Tile tile = tiles[blockIdx.x];
+    __shared__ float lds[kStreamWaves * kWave * V];
+    const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
     if (tile.kind == KIND_VECTOR) {
-        if (tile.dtype == DT_F32) elementwise_tile<float>(td, g, tile, k);
-        else elementwise_tile<uint16_t>(td, g, tile, k);
+        elementwise_tile<XT, kStreamThreads>(td, g, tile, k);
         return;
     }
-    if (tile.dtype == DT_F32) {
-        const float *gf = static_cast<const float *>(g);
-        if (tile.vec == 4) stream_matrix<float, 4>(td, gf, tile, ws, k, pending, lds);
-        else stream_matrix<float, 1>(td, gf, tile, ws, k, pending, lds);
-    } else {
-        const uint16_t *gb = static_cast<const uint16_t *>(g);
-        if (tile.vec == 8) stream_matrix<uint16_t, 8>(td, gb, tile, ws, k, pending, lds);
-        else if (tile.vec == 4) stream_matrix<uint16_t, 4>(td, gb, tile, ws, k, pending, lds);
-        else stream_matrix<uint16_t, 1>(td, gb, tile, ws, k, pending, lds);
-    }
+    stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
 }
 
 // Finalisation (C.2 / C.3 stage 2).  Row items: thread t owns row start+t,
 // sums its column-block partials in block order, updates R, and the
 // workgroup writes the fixed-order sum of its 256 new R values.  Column
-// items: 64 columns x 4 groups of row stripes, folded in group order.
+// items: cw columns x 256/cw groups of row stripes (more groups for taller
+// tensors), each group summing its stripes in order, groups folded in order.
 // init_only recomputes the partial sums of R from R as it stands.
 __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
     const TensorDesc *__restrict__ tensors, const FinItem *__restrict__ items,
@@ -372,9 +423,16 @@ __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
             const int64_t i = static_cast<int64_t>(it.start) + t;
             rv = gmem(td.r)[i];
             if (!init_only) {
-                const float *rp = ws + td.rowpart + i;
+                const RK_GLOBAL float *rp = gmem(ws) + td.rowpart + i;
                 float s = 0.f;
-                for (int cb = 0; cb < td.ncb; ++cb) s += gmem(rp)[static_cast<int64_t>(cb) * td.m];
+                for (int cb = 0; cb < td.ncb; cb += 8) {
+                    float v[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        v[q] = cb + q < td.ncb ? rp[static_cast<int64_t>(cb + q) * td.m] : 0.f;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) s += v[q];
+                }
                 rv = k.a * rv + k.kappa * s;
                 gmem(td.r)[i] = rv;
             }
@@ -391,20 +449,34 @@ __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
             if (!isfinite(s)) *gmem(flag) = 1;
         }
     } else {
-        const int j = threadIdx.x & (kWave - 1);
-        const int grp = threadIdx.x >> 6;
-        const int per = (td.nrs + kWaves - 1) / kWaves;
-        const int s0 = grp * per;
+        // cw = 2^cwlog columns x (256 / cw) groups of row stripes.
+        const int cwlog = it.cwlog;
+        const int cw = 1 << cwlog;
+        const int ngrp = kThreads >> cwlog;
+        const int j = threadIdx.x & (cw - 1);
+        const int grp = threadIdx.x >> cwlog;
+        const int per = (td.nrs + ngrp - 1) / ngrp;
+        const int s0 = min(td.nrs, grp * per);
         const int s1 = min(td.nrs, s0 + per);
         float s = 0.f;
         if (j < it.count) {
-            const float *cp = ws + td.colpart + it.start + j;
-            for (int st = s0; st < s1; ++st) s += gmem(cp)[static_cast<int64_t>(st) * td.n];
+            const RK_GLOBAL float *cp = gmem(ws) + td.colpart + it.start + j;
+            // Loads in batches of 16 (missing ones read as 0, which adds
+            // nothing), additions in stripe order.
+            for (int st = s0; st < s1; st += 16) {
+                float v[16];
+#pragma unroll
+                for (int q = 0; q < 16; ++q)
+                    v[q] = st + q < s1 ? cp[static_cast<int64_t>(st + q) * td.n] : 0.f;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) s += v[q];
+            }
         }
         lds[threadIdx.x] = s;
         __syncthreads();
         if (grp == 0 && j < it.count) {
-            const float cs = ((lds[j] + lds[kWave + j]) + lds[2 * kWave + j]) + lds[3 * kWave + j];
+            float cs = 0.f;
+            for (int q = 0; q < ngrp; ++q) cs += lds[q * cw + j];
             const int64_t jj = static_cast<int64_t>(it.start) + j;
             const float cvn = k.a * gmem(td.c)[jj] + k.kappa * cs;
             gmem(td.c)[jj] = cvn;
@@ -434,8 +506,8 @@ __device__ void apply_matrix(const TensorDesc &td, const Tile &tile, const float
 #pragma unroll
     for (int i = 0; i < V; ++i) cv[i] = colok ? gmem(td.c)[col + i] : 0.f;
     const float denom = sum_r(ws + td.chunk, td.nchunk) + k.eps;
-    const int64_t r0 = tile.start + static_cast<int64_t>(wave) * kRowsPerWave;
-    const int nr = max(0, min(kRowsPerWave, static_cast<int>(tile.start + tile.count - r0)));
+    const int64_t r0 = tile.start + static_cast<int64_t>(wave) * tile.rpw;
+    const int nr = max(0, min(tile.rpw, static_cast<int>(tile.start + tile.count - r0)));
     const float myrate = lane < nr ? row_rate(k.kh, gmem(td.r)[r0 + lane], denom) : 0.f;
     float *__restrict__ p = td.p;
     const int nld = (nr + G - 1) >> (6 - llog);
@@ -453,16 +525,15 @@ __device__ void apply_matrix(const TensorDesc &td, const Tile &tile, const float
     }
 }
 
-__global__ __launch_bounds__(kThreads) void rikfad_apply_kernel(
-    const TensorDesc *__restrict__ tensors, const Tile *__restrict__ tiles,
+template <int V>
+__global__ __launch_bounds__(kStreamThreads) void rikfad_apply_kernel(
+    const TensorDesc *__restrict__ tensors, const Tile *__restrict__ tiles, int64_t tile0,
     const float *__restrict__ ws, Coeffs k)
 {
-    const Tile tile = tiles[blockIdx.x];
+    const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     if (tile.kind != KIND_MATRIX) return;
-    if (tile.vec == 8) apply_matrix<8>(td, tile, ws, k);
-    else if (tile.vec == 4) apply_matrix<4>(td, tile, ws, k);
-    else apply_matrix<1>(td, tile, ws, k);
+    apply_matrix<V>(td, tile, ws, k);
 }
 
 // Full-tensor iKFAD: every tile is an element range with its own friction.
@@ -473,42 +544,84 @@ __global__ __launch_bounds__(kThreads) void ikfad_kernel(
     const Tile tile = tiles[blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
-    if (tile.dtype == DT_F32) elementwise_tile<float>(td, g, tile, k);
-    else elementwise_tile<uint16_t>(td, g, tile, k);
+    if (tile.dtype == DT_F32) elementwise_tile<float, kThreads>(td, g, tile, k);
+    else elementwise_tile<uint16_t, kThreads>(td, g, tile, k);
 }
 
 // ------------------------------------------------------------- probes
 
+// Each workgroup streams 4 KB per operand: four 16-byte non-temporal
+// accesses per thread, all loads issued before any store.
+constexpr int kProbeUnroll = 4;
+
 __global__ __launch_bounds__(kThreads) void probe_stream_kernel(
-    const float4 *__restrict__ a, const float4 *__restrict__ b, const float4 *__restrict__ c,
-    float4 *__restrict__ d, float4 *__restrict__ e, int64_t n4)
+    const f32x4 *__restrict__ a, const f32x4 *__restrict__ b, const f32x4 *__restrict__ c,
+    f32x4 *__restrict__ d, f32x4 *__restrict__ e, int64_t n4)
 {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n4;
-         i += static_cast<int64_t>(gridDim.x) * kThreads) {
-        const float4 va = a[i], vb = b[i], vc = c[i];
-        d[i] = make_float4(va.x + vb.x, va.y + vb.y, va.z + vb.z, va.w + vb.w);
-        e[i] = make_float4(va.x * vc.x, va.y * vc.y, va.z * vc.z, va.w * vc.w);
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * kProbeUnroll + threadIdx.x;
+    f32x4 va[kProbeUnroll], vb[kProbeUnroll], vc[kProbeUnroll];
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n4) {
+            va[u] = ldg(a + i);
+            vb[u] = ldg(b + i);
+            vc[u] = ldg(c + i);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n4) {
+            stg(d + i, va[u] + vb[u]);
+            stg(e + i, va[u] * vc[u]);
+        }
     }
 }
 
 __global__ __launch_bounds__(kThreads) void probe_copy_kernel(
-    const uint4 *__restrict__ s, uint4 *__restrict__ d, int64_t n16)
+    const u32x4 *__restrict__ s, u32x4 *__restrict__ d, int64_t n16)
 {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n16;
-         i += static_cast<int64_t>(gridDim.x) * kThreads)
-        d[i] = s[i];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * kProbeUnroll + threadIdx.x;
+    u32x4 v[kProbeUnroll];
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n16) v[u] = ldg(s + i);
+    }
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n16) stg(d + i, v[u]);
+    }
 }
 
 // ------------------------------------------------------------- launchers
 
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                         int64_t ntiles, float *ws, const Coeffs &k, int pending,
-                         hipStream_t stream)
+                         const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
+                         int pending, hipStream_t stream)
 {
-    if (ntiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rikfad_stream_kernel, dim3(static_cast<uint32_t>(ntiles)), dim3(kThreads),
-                       0, stream, tensors, grads, tiles, ws, k, pending);
-    return hipGetLastError();
+    for (int q = 0; q < ngroups; ++q) {
+        const TileGroup &gr = groups[q];
+        if (gr.count <= 0) continue;
+        const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
+#define RK_LAUNCH(XT, V)                                                                     \
+    hipLaunchKernelGGL((rikfad_stream_kernel<XT, V>), grid, block, 0, stream, tensors, grads, \
+                       tiles, gr.begin, ws, k, pending)
+        if (gr.dtype == DT_F32) {
+            if (gr.vec == 4) RK_LAUNCH(float, 4);
+            else RK_LAUNCH(float, 1);
+        } else {
+            if (gr.vec == 8) RK_LAUNCH(uint16_t, 8);
+            else if (gr.vec == 4) RK_LAUNCH(uint16_t, 4);
+            else RK_LAUNCH(uint16_t, 1);
+        }
+#undef RK_LAUNCH
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
@@ -521,13 +634,26 @@ hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int6
     return hipGetLastError();
 }
 
-hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, int64_t ntiles,
-                        const float *ws, const Coeffs &k, hipStream_t stream)
+hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,
+                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream)
 {
-    if (ntiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rikfad_apply_kernel, dim3(static_cast<uint32_t>(ntiles)), dim3(kThreads),
-                       0, stream, tensors, tiles, ws, k);
-    return hipGetLastError();
+    for (int q = 0; q < ngroups; ++q) {
+        const TileGroup &gr = groups[q];
+        if (gr.count <= 0) continue;
+        const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
+        if (gr.vec == 8)
+            hipLaunchKernelGGL(rikfad_apply_kernel<8>, grid, block, 0, stream, tensors, tiles,
+                               gr.begin, ws, k);
+        else if (gr.vec == 4)
+            hipLaunchKernelGGL(rikfad_apply_kernel<4>, grid, block, 0, stream, tensors, tiles,
+                               gr.begin, ws, k);
+        else
+            hipLaunchKernelGGL(rikfad_apply_kernel<1>, grid, block, 0, stream, tensors, tiles,
+                               gr.begin, ws, k);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
@@ -541,9 +667,8 @@ hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, con
 
 static uint32_t probe_grid(int64_t units)
 {
-    const int64_t want = (units + kThreads - 1) / kThreads;
-    const int64_t cap = 256 * 32;     // 32 workgroups per CU on 256 CUs
-    return static_cast<uint32_t>(want < 1 ? 1 : (want < cap ? want : cap));
+    const int64_t per = int64_t(kThreads) * kProbeUnroll;
+    return static_cast<uint32_t>((units + per - 1) / per);
 }
 
 hipError_t launch_probe_stream(const float *a, const float *b, const float *c, float *d,
@@ -552,9 +677,9 @@ hipError_t launch_probe_stream(const float *a, const float *b, const float *c, f
     const int64_t n4 = nfloat / 4;
     if (n4 <= 0) return hipSuccess;
     hipLaunchKernelGGL(probe_stream_kernel, dim3(probe_grid(n4)), dim3(kThreads), 0, stream,
-                       reinterpret_cast<const float4 *>(a), reinterpret_cast<const float4 *>(b),
-                       reinterpret_cast<const float4 *>(c), reinterpret_cast<float4 *>(d),
-                       reinterpret_cast<float4 *>(e), n4);
+                       reinterpret_cast<const f32x4 *>(a), reinterpret_cast<const f32x4 *>(b),
+                       reinterpret_cast<const f32x4 *>(c), reinterpret_cast<f32x4 *>(d),
+                       reinterpret_cast<f32x4 *>(e), n4);
     return hipGetLastError();
 }
 
@@ -563,7 +688,7 @@ hipError_t launch_probe_copy(const void *s, void *d, int64_t nbytes, hipStream_t
     const int64_t n16 = nbytes / 16;
     if (n16 <= 0) return hipSuccess;
     hipLaunchKernelGGL(probe_copy_kernel, dim3(probe_grid(n16)), dim3(kThreads), 0, stream,
-                       static_cast<const uint4 *>(s), static_cast<uint4 *>(d), n16);
+                       static_cast<const u32x4 *>(s), static_cast<u32x4 *>(d), n16);
     return hipGetLastError();
 }
 

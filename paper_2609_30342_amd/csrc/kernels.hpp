@@ -7,19 +7,20 @@
 
 namespace rk {
 
-// Streaming pass over all tiles (matrix and vector) of a context.
+// Streaming pass over all tiles (matrix and vector) of a context: one
+// launch per tile group.
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                         int64_t ntiles, float *ws, const Coeffs &k, int pending,
-                         hipStream_t stream);
+                         const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
+                         int pending, hipStream_t stream);
 
 // Finalisation of R, C and the partial sums of R (init_only: sums only).
 hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
                            float *ws, const Coeffs &k, int *flag, int init_only,
                            hipStream_t stream);
 
-// Second half-kick + D over matrix tiles.
-hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, int64_t ntiles,
-                        const float *ws, const Coeffs &k, hipStream_t stream);
+// Second half-kick + D over the matrix tiles of every tile group.
+hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,
+                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream);
 
 // Full-tensor element-wise iKFAD.
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,

@@ -8,13 +8,27 @@
 
 namespace rk {
 
+#ifndef RK_STREAM_WAVES
+#define RK_STREAM_WAVES 8
+#endif
 constexpr int kWave = 64;                       // CDNA wavefront
-constexpr int kWaves = 4;                       // waves per workgroup
-constexpr int kThreads = kWave * kWaves;        // 256
-constexpr int kRowsPerWave = 64;                // lane t keeps row t's partial sum
-constexpr int kStripeRows = kWaves * kRowsPerWave;  // rows per matrix tile
+constexpr int kThreads = 256;                   // workgroup of the small kernels
+constexpr int kStreamWaves = RK_STREAM_WAVES;   // waves per streaming workgroup
+constexpr int kStreamThreads = kWave * kStreamWaves;
+#ifndef RK_BATCH
+#define RK_BATCH 2
+#endif
+#ifndef RK_BLOCK_LANES
+#define RK_BLOCK_LANES 64
+#endif
+#ifndef RK_ROWS_PER_WAVE
+#define RK_ROWS_PER_WAVE 4
+#endif
+constexpr int kBatch = RK_BATCH;                // row loads in flight per wave
+constexpr int kMaxRowsPerWave = 64;             // lane t keeps row t's partial sum
+constexpr int kBlockLanes = RK_BLOCK_LANES;     // lanes per row of a full column block
+constexpr int kRowsPerWave = RK_ROWS_PER_WAVE;  // rows per wave of a matrix tile
 constexpr int kChunkRows = kThreads;            // rows per finalisation item
-constexpr int kColItem = kWave;                 // columns per finalisation item
 constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kVecIters
 
 enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
@@ -40,7 +54,7 @@ struct TensorDesc {
 struct Tile {
     int64_t start;     // matrix: first row; vector: first element
     int32_t tensor;
-    int32_t count;     // matrix: rows (<= kStripeRows); vector: elements
+    int32_t count;     // matrix: rows (<= kStreamWaves * rpw); vector: elements
     int32_t col0;      // matrix: first column of the block
     int32_t ncols;     // matrix: columns of the block (multiple of vec)
     int32_t stripe;    // matrix: row-stripe index (row of the column partials)
@@ -49,6 +63,18 @@ struct Tile {
     int32_t kind;
     int32_t vec;       // elements per lane access: 1, 4 or 8
     int32_t dtype;
+    int32_t rpw;       // matrix: rows per wave (<= kMaxRowsPerWave)
+    int32_t pad;
+};
+
+// A contiguous range of the tile table served by one launch of the
+// streaming kernel instantiated for the (dtype, vec) of its matrix tiles.
+// Vector tiles of the same dtype are appended to one group of that dtype.
+struct TileGroup {
+    int32_t dtype;
+    int32_t vec;
+    int64_t begin;
+    int64_t count;
 };
 
 // One workgroup of the finalisation pass.
@@ -56,9 +82,9 @@ struct FinItem {
     int32_t tensor;
     int32_t kind;      // FIN_ROWS or FIN_COLS
     int32_t start;     // first row / column
-    int32_t count;     // rows (<= kChunkRows) / columns (<= kColItem)
+    int32_t count;     // rows (<= kChunkRows) / columns (<= 64)
     int32_t chunk;     // FIN_ROWS: which partial sum of R this item writes
-    int32_t pad;
+    int32_t cwlog;     // FIN_COLS: log2 of columns per item (threads: cw x 256/cw)
 };
 
 // Step coefficients, computed in fp64 on the host and rounded once.

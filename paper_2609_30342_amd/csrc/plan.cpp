@@ -23,7 +23,12 @@ int32_t matrix_vec(const rikfad_tensor &t)
 {
     if (t.dtype == RIKFAD_FP32)
         return (t.n % 4 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) ? 4 : 1;
-    if (t.n % 8 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) return 8;
+#ifndef RK_BF16_MAXVEC
+#define RK_BF16_MAXVEC 4
+#endif
+    if (RK_BF16_MAXVEC >= 8 && t.n % 8 == 0 && aligned(t.x, 16) && aligned(t.g, 16) &&
+        aligned(t.p, 16))
+        return 8;
     if (t.n % 4 == 0 && aligned(t.x, 8) && aligned(t.g, 8) && aligned(t.p, 16)) return 4;
     return 1;
 }
@@ -149,7 +154,12 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     int64_t ws = 0;
     pl.tensors.resize(static_cast<size_t>(count));
     pl.grads.resize(static_cast<size_t>(count));
-    std::vector<Tile> vec_tiles;
+    // Matrix tiles by launch class (fp32 v4, fp32 v1, bf16 v8, bf16 v4,
+    // bf16 v1); vector tiles by dtype.
+    const int32_t class_dtype[5] = {DT_F32, DT_F32, DT_BF16, DT_BF16, DT_BF16};
+    const int32_t class_vec[5] = {4, 1, 8, 4, 1};
+    std::vector<Tile> mat_tiles[5];
+    std::vector<Tile> vec_tiles[2];
     std::vector<FinItem> col_items;
     for (int64_t i = 0; i < count; ++i) {
         const rikfad_tensor &T = t[i];
@@ -177,7 +187,8 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
             pl.stream_min_bytes += mn * (3 * eb + 16);
             Plan tmp;
             add_flat_tiles(tmp, static_cast<int32_t>(i), mn, T.dtype, d.vec);
-            vec_tiles.insert(vec_tiles.end(), tmp.tiles.begin(), tmp.tiles.end());
+            std::vector<Tile> &vt = vec_tiles[T.dtype == DT_F32 ? 0 : 1];
+            vt.insert(vt.end(), tmp.tiles.begin(), tmp.tiles.end());
             continue;
         }
         d.kind = KIND_MATRIX;
@@ -187,22 +198,31 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         pl.min_bytes += mn * (3 * eb + 8) + 8 * (T.m + T.n);   // x g p in, x p out; R C
         pl.stream_min_bytes += mn * (3 * eb + 8) + 4 * (T.m + T.n); // R, C read only
 
-        // Column blocks of up to 64 lanes x vec columns; a narrow last block
-        // uses the smallest power-of-two lane count that covers it.
+        // Column blocks of kBlockLanes lanes x vec columns; a narrow last
+        // block uses the smallest power-of-two lane count that covers it.
+        // Tiles are kStreamWaves waves x rpw rows: rpw grows for narrow
+        // blocks so that every tile has about the same number of accesses.
         struct Block { int32_t col0, ncols, llog; };
         std::vector<Block> blocks;
+        int blog = 0;
+        while ((1 << blog) < kBlockLanes) ++blog;
         const int64_t lanes = T.n / d.vec;
-        const int64_t full = lanes / kWave, rem = lanes % kWave;
+        const int64_t full = lanes >> blog, rem = lanes & ((int64_t(1) << blog) - 1);
         for (int64_t b = 0; b < full; ++b)
-            blocks.push_back({static_cast<int32_t>(b * kWave * d.vec), kWave * d.vec, 6});
+            blocks.push_back({static_cast<int32_t>((b << blog) * d.vec),
+                              static_cast<int32_t>((int64_t(1) << blog) * d.vec), blog});
         if (rem > 0) {
             int llog = 0;
             while ((int64_t(1) << llog) < rem) ++llog;
-            blocks.push_back({static_cast<int32_t>(full * kWave * d.vec),
+            blocks.push_back({static_cast<int32_t>((full << blog) * d.vec),
                               static_cast<int32_t>(rem * d.vec), llog});
         }
+        const int lead_llog = blocks.front().llog;
+        int rpw = kRowsPerWave << (blog - (lead_llog < blog ? lead_llog : blog));
+        if (rpw > kMaxRowsPerWave) rpw = kMaxRowsPerWave;
+        const int64_t stripe_rows = int64_t(kStreamWaves) * rpw;
         d.ncb = static_cast<int32_t>(blocks.size());
-        d.nrs = static_cast<int32_t>(ceil_div(T.m, kStripeRows));
+        d.nrs = static_cast<int32_t>(ceil_div(T.m, stripe_rows));
         d.nchunk = static_cast<int32_t>(ceil_div(T.m, kChunkRows));
         d.rowpart = ws;
         ws += round_up(T.m * d.ncb, 64);
@@ -211,13 +231,15 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         d.chunk = ws;
         ws += round_up(d.nchunk, 64);
 
+        int cls = 0;
+        while (!(class_dtype[cls] == T.dtype && class_vec[cls] == d.vec)) ++cls;
         for (int32_t s = 0; s < d.nrs; ++s) {
             for (int32_t b = 0; b < d.ncb; ++b) {
                 Tile tl{};
-                tl.start = int64_t(s) * kStripeRows;
+                tl.start = int64_t(s) * stripe_rows;
                 tl.tensor = static_cast<int32_t>(i);
                 tl.count = static_cast<int32_t>(
-                    T.m - tl.start < kStripeRows ? T.m - tl.start : kStripeRows);
+                    T.m - tl.start < stripe_rows ? T.m - tl.start : stripe_rows);
                 tl.col0 = blocks[static_cast<size_t>(b)].col0;
                 tl.ncols = blocks[static_cast<size_t>(b)].ncols;
                 tl.stripe = s;
@@ -226,7 +248,8 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                 tl.kind = KIND_MATRIX;
                 tl.vec = d.vec;
                 tl.dtype = T.dtype;
-                pl.tiles.push_back(tl);
+                tl.rpw = rpw;
+                mat_tiles[cls].push_back(tl);
             }
         }
         for (int32_t q = 0; q < d.nchunk; ++q) {
@@ -235,13 +258,37 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                               static_cast<int32_t>(T.m - r0 < kChunkRows ? T.m - r0 : kChunkRows),
                               q, 0});
         }
-        for (int64_t j0 = 0; j0 < T.n; j0 += kColItem)
+        // Column items: cw columns x 256/cw groups of stripes, with enough
+        // groups that each thread sums at most about 32 stripe partials.
+        int cwlog = 6;
+        while (cwlog > 2 && ceil_div(d.nrs, kThreads >> cwlog) > 32) --cwlog;
+        const int64_t cw = int64_t(1) << cwlog;
+        for (int64_t j0 = 0; j0 < T.n; j0 += cw)
             col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
-                                 static_cast<int32_t>(T.n - j0 < kColItem ? T.n - j0 : kColItem),
-                                 0, 0});
+                                 static_cast<int32_t>(T.n - j0 < cw ? T.n - j0 : cw), 0,
+                                 cwlog});
     }
-    pl.matrix_tiles = static_cast<int64_t>(pl.tiles.size());
-    pl.tiles.insert(pl.tiles.end(), vec_tiles.begin(), vec_tiles.end());
+    bool vec_placed[2] = {false, false};
+    for (int cls = 0; cls < 5; ++cls) {
+        if (mat_tiles[cls].empty()) continue;
+        const int dt = class_dtype[cls] == DT_F32 ? 0 : 1;
+        TileGroup gr{class_dtype[cls], class_vec[cls], static_cast<int64_t>(pl.tiles.size()), 0};
+        pl.tiles.insert(pl.tiles.end(), mat_tiles[cls].begin(), mat_tiles[cls].end());
+        pl.matrix_tiles += static_cast<int64_t>(mat_tiles[cls].size());
+        if (!vec_placed[dt]) {
+            pl.tiles.insert(pl.tiles.end(), vec_tiles[dt].begin(), vec_tiles[dt].end());
+            vec_placed[dt] = true;
+        }
+        gr.count = static_cast<int64_t>(pl.tiles.size()) - gr.begin;
+        pl.groups.push_back(gr);
+    }
+    for (int dt = 0; dt < 2; ++dt) {
+        if (vec_placed[dt] || vec_tiles[dt].empty()) continue;
+        TileGroup gr{dt == 0 ? DT_F32 : DT_BF16, 1, static_cast<int64_t>(pl.tiles.size()),
+                     static_cast<int64_t>(vec_tiles[dt].size())};
+        pl.tiles.insert(pl.tiles.end(), vec_tiles[dt].begin(), vec_tiles[dt].end());
+        pl.groups.push_back(gr);
+    }
     pl.row_items = static_cast<int64_t>(pl.fin.size());
     pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());
     pl.ws_floats = ws;

@@ -14,7 +14,8 @@ namespace rk {
 struct Plan {
     std::vector<TensorDesc> tensors;
     std::vector<const void *> grads;
-    std::vector<Tile> tiles;          // matrix tiles first, then vector tiles
+    std::vector<Tile> tiles;          // grouped by (dtype, vec); see TileGroup
+    std::vector<TileGroup> groups;    // one streaming launch each
     int64_t matrix_tiles = 0;
     std::vector<FinItem> fin;         // row items first, then column items
     int64_t row_items = 0;
