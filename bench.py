@@ -51,11 +51,12 @@ def measured_traffic(dtype):
 
 
 def build_workload(specs, dtype, seed, device):
+    """dtype None: each tensor in its own spec's storage type."""
     import torch
     gen = torch.Generator(device=device).manual_seed(seed)
-    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
     xs, gs = [], []
     for sp in specs:
+        dt = torch.bfloat16 if (dtype or sp.dtype) == "bf16" else torch.float32
         x = (torch.randn((sp.m, sp.n), generator=gen, device=device) * 0.02).to(dt)
         s = torch.exp(0.5 * torch.randn(sp.m, generator=gen, device=device))
         t = torch.exp(0.5 * torch.randn(sp.n, generator=gen, device=device))
@@ -117,6 +118,42 @@ def time_ikfad(specs, hp, steps, warmup, seed=0):
     return ms / n
 
 
+def time_small(specs, hp, steps, warmup, seed=0):
+    """Launch-bound parameter sets: microseconds per step issued eagerly and
+    replayed from a HIP graph that holds one captured step."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    xs, gs = build_workload(specs, None, seed, torch.device("cuda:0"))
+    opt = R.RIKFAD(xs, gs, **hp)
+    for _ in range(warmup):
+        opt.step()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        opt.step()
+    b.record()
+    torch.cuda.synchronize()
+    eager = a.elapsed_time(b) / steps
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        opt.step()
+    g.replay()
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(steps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    graph = a.elapsed_time(b) / steps
+    n = sum(sp.numel for sp in specs)
+    opt.close()
+    del g, xs, gs
+    torch.cuda.empty_cache()
+    return {"params": n, "eager_us": eager * 1e3, "graph_us": graph * 1e3,
+            "graph_params_per_s": n / (graph * 1e-3)}
+
+
 def time_probe(nfloat, reps=10):
     """3-read / 2-write fp32 stream of the same byte count as the step."""
     import torch
@@ -173,8 +210,8 @@ def cpu_baseline(specs, hp, budget_s):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for cpu_baseline (0 = skip)")
@@ -259,6 +296,11 @@ def main():
                                       "hbm_gbps": 28.0 * N / (ik_ms * 1e-3) / 1e9,
                                       "state_bytes": info["ikfad_state_bytes"]}
         var["probe_3r2w_gbps"] = time_probe(N)
+        var["launch_bound_sets"] = {
+            "single_256x512_fp32": time_small(synth.single_matrix(), hp, 200, 5),
+            "gpt2_nano_fp32": time_small(synth.gpt2_nano(), hp, 100, 5),
+            "tinyvit_bf16": time_small(synth.tinyvit_like(), hp, 100, 5),
+        }
         out["variants"] = var
     if args.calibrate_copy_mib > 0:
         nbytes = args.calibrate_copy_mib << 20

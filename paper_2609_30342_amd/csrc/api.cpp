@@ -271,9 +271,15 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
     ctx->pending = false;
     if (tm.on && (s = tm.mark(tm.steps, 1, stream)) != RIKFAD_OK) return s;
-    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, static_cast<int64_t>(pl.fin.size()),
-                            ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream);
+    const int64_t nfin = static_cast<int64_t>(pl.fin.size());
+    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin - pl.fold_items, ctx->dev.ws,
+                            ctx->k, ctx->dev.flag, 0, stream);
     if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
+    if (pl.fold_items > 0) {
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + (nfin - pl.fold_items),
+                                pl.fold_items, ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
+    }
     if (tm.on && (s = tm.mark(tm.steps, 2, stream)) != RIKFAD_OK) return s;
     ctx->pending = pl.matrix_tiles > 0;
     if (ctx->two_pass && (s = apply_pending(ctx, stream)) != RIKFAD_OK) return s;

@@ -50,6 +50,9 @@ __device__ __forceinline__ RK_GLOBAL T *gmem(T *q)
 #ifndef RK_NT
 #define RK_NT 1
 #endif
+#ifndef RK_PERSIST
+#define RK_PERSIST 0
+#endif
 
 template <typename T>
 __device__ __forceinline__ T ldg(const T *q)
@@ -174,6 +177,67 @@ template <> struct Io<uint16_t, 1> {
     static __device__ __forceinline__ void store(uint16_t *q, const float (&o)[1]) { stg(q, f32_to_bf16(o[0])); }
 };
 
+// Raw<T, V>: the V elements of one lane access as loaded (packed bf16 stays
+// packed in registers until it is used).
+template <typename T, int V> struct Raw;
+
+template <> struct Raw<float, 4> {
+    typedef f32x4 type;
+    static __device__ __forceinline__ type load(const float *q)
+    {
+        return ldg(reinterpret_cast<const f32x4 *>(q));
+    }
+    static __device__ __forceinline__ void unpack(const type &v, float (&o)[4])
+    {
+        o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+    }
+};
+
+template <> struct Raw<float, 1> {
+    typedef float type;
+    static __device__ __forceinline__ type load(const float *q) { return ldg(q); }
+    static __device__ __forceinline__ void unpack(const type &v, float (&o)[1]) { o[0] = v; }
+};
+
+template <> struct Raw<uint16_t, 8> {
+    typedef u32x4 type;
+    static __device__ __forceinline__ type load(const uint16_t *q)
+    {
+        return ldg(reinterpret_cast<const u32x4 *>(q));
+    }
+    static __device__ __forceinline__ void unpack(const type &v, float (&o)[8])
+    {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o[2 * i] = __uint_as_float(w[i] << 16);
+            o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+};
+
+template <> struct Raw<uint16_t, 4> {
+    typedef u32x2 type;
+    static __device__ __forceinline__ type load(const uint16_t *q)
+    {
+        return ldg(reinterpret_cast<const u32x2 *>(q));
+    }
+    static __device__ __forceinline__ void unpack(const type &v, float (&o)[4])
+    {
+        o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
+        o[2] = __uint_as_float(v.y << 16); o[3] = __uint_as_float(v.y & 0xffff0000u);
+    }
+};
+
+template <> struct Raw<uint16_t, 1> {
+    typedef uint16_t type;
+    static __device__ __forceinline__ type load(const uint16_t *q) { return ldg(q); }
+    static __device__ __forceinline__ void unpack(const type &v, float (&o)[1])
+    {
+        o[0] = bf16_to_f32(v);
+    }
+};
+
 // ---------------------------------------------------------- reductions
 
 // Sum of the partial sums of R written by the finalisation pass.  Every
@@ -211,19 +275,25 @@ __device__ __forceinline__ float row_rate(float kh, float r_i, float denom)
 template <typename XT, int V>
 __device__ __forceinline__ void load_row(const XT *x, const XT *g, const float *p, int64_t r0,
                                          int64_t n, int64_t col, bool ok, int rl,
-                                         float (&xs)[V], float (&gs)[V], float (&qs)[V])
+                                         typename Raw<XT, V>::type &xs,
+                                         typename Raw<XT, V>::type &gs, float (&qs)[V])
 {
     const int64_t off = ok ? (r0 + rl) * n + col : r0 * n + col;
-    Io<XT, V>::load(x + off, xs);
-    Io<XT, V>::load(g + off, gs);
+    xs = Raw<XT, V>::load(x + off);
+    gs = Raw<XT, V>::load(g + off);
     Io<float, V>::load(p + off, qs);
 }
+
+// Depth of the per-wave ring of row loads (rows held per slot: x, g, p).
+template <typename XT> struct RingDepth { static constexpr int value = kRingF32; };
+template <> struct RingDepth<uint16_t> { static constexpr int value = kRingBF16; };
 
 template <typename XT, int V>
 __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
                               const Tile &tile, float *__restrict__ ws,
                               const Coeffs &k, int pending, float *lds)
 {
+    constexpr int B = RingDepth<XT>::value;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x >> 6;
     const int llog = tile.lanes_log2;
@@ -241,18 +311,19 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     XT *__restrict__ x = static_cast<XT *>(td.x);
     float *__restrict__ p = td.p;
 
-    // Ring of kBatch row loads: the load of row-load ld + kBatch is issued
-    // as soon as row-load ld has been consumed, so every wave keeps kBatch
+    // Ring of B row loads: the load of row-load ld + B is issued as soon
+    // as row-load ld has been consumed, so every wave keeps B
     // 1 KB requests per stream in flight.  The first loads go out before
     // the factor sum is read, hiding its latency.
-    float xv[kBatch][V], gv[kBatch][V], qv[kBatch][V];
+    typename Raw<XT, V>::type xr[B], gr[B];
+    float qv[B][V];
     // A lane outside the block's columns reads the block's first column.
     const int64_t lcol = colok ? col : tile.col0;
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u)
+    for (int u = 0; u < B; ++u)
         if (nr > 0)
-            load_row<XT, V>(x, g, p, r0, n, lcol, colok && u * G + seg < nr, u * G + seg, xv[u],
-                            gv[u], qv[u]);
+            load_row<XT, V>(x, g, p, r0, n, lcol, colok && u * G + seg < nr, u * G + seg, xr[u],
+                            gr[u], qv[u]);
 
     float cv[V];
 #pragma unroll
@@ -265,22 +336,25 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
     float myrow = 0.f;
 
-    for (int ld0 = 0; ld0 < nld; ld0 += kBatch) {
+    for (int ld0 = 0; ld0 < nld; ld0 += B) {
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < B; ++u) {
             const int ld = ld0 + u;
             const int rl = ld * G + seg;
             const bool ok = colok && rl < nr;
             const float rate = __shfl(myrate, rl & (kWave - 1));
+            float xv[V], gv[V];
+            Raw<XT, V>::unpack(xr[u], xv);
+            Raw<XT, V>::unpack(gr[u], gv);
             float rs = 0.f;
 #pragma unroll
             for (int i = 0; i < V; ++i) {
                 const float q = ok ? qv[u][i] : 0.f;
-                const float gg = ok ? gv[u][i] : 0.f;
+                const float gg = ok ? gv[i] : 0.f;
                 const float e = exp2f(rate * cv[i]);
                 const float pn = pending ? k.d * (q * e) : q;
                 const float pb = pn - k.h * gg;
-                xv[u][i] = xv[u][i] + k.h * pb;
+                xv[i] = xv[i] + k.h * pb;
                 const float p1 = pb * e;
                 qv[u][i] = p1;
                 const float sq = ok ? p1 * p1 : 0.f;
@@ -289,12 +363,12 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
             }
             if (ok) {
                 const int64_t off = (r0 + rl) * n + col;
-                Io<XT, V>::store(x + off, xv[u]);
+                Io<XT, V>::store(x + off, xv);
                 Io<float, V>::store(p + off, qv[u]);
             }
-            const int rn = (ld + kBatch) * G + seg;
-            if (ld + kBatch < nld)
-                load_row<XT, V>(x, g, p, r0, n, lcol, colok && rn < nr, rn, xv[u], gv[u], qv[u]);
+            const int rn = (ld + B) * G + seg;
+            if (ld + B < nld)
+                load_row<XT, V>(x, g, p, r0, n, lcol, colok && rn < nr, rn, xr[u], gr[u], qv[u]);
             for (int o = 1; o < L; o <<= 1) rs += __shfl_xor(rs, o);
             const int first = ld * G;                 // first row of this load
             const float v = __shfl(rs, ((lane - first) & (G - 1)) << llog);
@@ -389,10 +463,23 @@ __device__ void elementwise_tile(const TensorDesc &td, const void *g, const Tile
 template <typename XT, int V>
 __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
-    const Tile *__restrict__ tiles, int64_t tile0, float *__restrict__ ws, Coeffs k,
-    int pending)
+    const Tile *__restrict__ tiles, int64_t tile0, int64_t ntile, float *__restrict__ ws,
+    Coeffs k, int pending)
 {
     __shared__ float lds[kStreamWaves * kWave * V];
+#if RK_PERSIST
+    for (int64_t t = blockIdx.x; t < ntile; t += gridDim.x) {
+        const Tile tile = tiles[tile0 + t];
+        const TensorDesc td = tensors[tile.tensor];
+        const void *g = grads[tile.tensor];
+        if (tile.kind == KIND_VECTOR) {
+            elementwise_tile<XT, kStreamThreads>(td, g, tile, k);
+        } else {
+            stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
+        }
+        __syncthreads();
+    }
+#else
     const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
@@ -401,13 +488,14 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
         return;
     }
     stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
+#endif
 }
 
 // Finalisation (C.2 / C.3 stage 2).  Row items: thread t owns row start+t,
 // sums its column-block partials in block order, updates R, and the
 // workgroup writes the fixed-order sum of its 256 new R values.  Column
-// items: cw columns x 256/cw groups of row stripes (more groups for taller
-// tensors), each group summing its stripes in order, groups folded in order.
+// items sum one segment of row stripes for 64 columns; tall tensors have
+// several segments, folded in segment order by a second, small launch.
 // init_only recomputes the partial sums of R from R as it stands.
 __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
     const TensorDesc *__restrict__ tensors, const FinItem *__restrict__ items,
@@ -448,36 +536,54 @@ __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
             gmem(ws)[td.chunk + it.chunk] = s;
             if (!isfinite(s)) *gmem(flag) = 1;
         }
-    } else {
-        // cw = 2^cwlog columns x (256 / cw) groups of row stripes.
-        const int cwlog = it.cwlog;
-        const int cw = 1 << cwlog;
-        const int ngrp = kThreads >> cwlog;
-        const int j = threadIdx.x & (cw - 1);
-        const int grp = threadIdx.x >> cwlog;
-        const int per = (td.nrs + ngrp - 1) / ngrp;
-        const int s0 = min(td.nrs, grp * per);
-        const int s1 = min(td.nrs, s0 + per);
+    } else if (it.kind == FIN_COLS) {
+        // Wave q sums stripes [seg0 + 16 q, seg0 + 16 q + 16) of the 64
+        // columns (each load a coalesced 256-byte row), in stripe order;
+        // the four waves are folded in wave order.
+        const int j = threadIdx.x & (kWave - 1);
+        const int q = threadIdx.x >> 6;
+        const int seg0 = it.chunk * kSegStripes;
+        const int s0 = min(td.nrs, seg0 + q * (kSegStripes / 4));
+        const int s1 = min(td.nrs, s0 + kSegStripes / 4);
         float s = 0.f;
         if (j < it.count) {
             const RK_GLOBAL float *cp = gmem(ws) + td.colpart + it.start + j;
-            // Loads in batches of 16 (missing ones read as 0, which adds
-            // nothing), additions in stripe order.
-            for (int st = s0; st < s1; st += 16) {
-                float v[16];
+            float v[kSegStripes / 4];
 #pragma unroll
-                for (int q = 0; q < 16; ++q)
-                    v[q] = st + q < s1 ? cp[static_cast<int64_t>(st + q) * td.n] : 0.f;
+            for (int u = 0; u < kSegStripes / 4; ++u)
+                v[u] = s0 + u < s1 ? cp[static_cast<int64_t>(s0 + u) * td.n] : 0.f;
 #pragma unroll
-                for (int q = 0; q < 16; ++q) s += v[q];
-            }
+            for (int u = 0; u < kSegStripes / 4; ++u) s += v[u];
         }
         lds[threadIdx.x] = s;
         __syncthreads();
-        if (grp == 0 && j < it.count) {
-            float cs = 0.f;
-            for (int q = 0; q < ngrp; ++q) cs += lds[q * cw + j];
+        if (q == 0 && j < it.count) {
+            const float cs = ((lds[j] + lds[kWave + j]) + lds[2 * kWave + j]) + lds[3 * kWave + j];
             const int64_t jj = static_cast<int64_t>(it.start) + j;
+            if (td.nseg > 1) {
+                gmem(ws)[td.colseg + static_cast<int64_t>(it.chunk) * td.n + jj] = cs;
+            } else {
+                const float cvn = k.a * gmem(td.c)[jj] + k.kappa * cs;
+                gmem(td.c)[jj] = cvn;
+                if (!isfinite(cvn)) *gmem(flag) = 1;
+            }
+        }
+    } else {
+        // FIN_FOLD: thread t owns column start + t and adds its segment sums
+        // in segment order.
+        const int t = threadIdx.x;
+        if (t < it.count) {
+            const int64_t jj = static_cast<int64_t>(it.start) + t;
+            const RK_GLOBAL float *sp = gmem(ws) + td.colseg + jj;
+            float cs = 0.f;
+            for (int q0 = 0; q0 < td.nseg; q0 += 16) {
+                float v[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u)
+                    v[u] = q0 + u < td.nseg ? sp[static_cast<int64_t>(q0 + u) * td.n] : 0.f;
+#pragma unroll
+                for (int u = 0; u < 16; ++u) cs += v[u];
+            }
             const float cvn = k.a * gmem(td.c)[jj] + k.kappa * cs;
             gmem(td.c)[jj] = cvn;
             if (!isfinite(cvn)) *gmem(flag) = 1;
@@ -605,10 +711,15 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
+#if RK_PERSIST
+        const int64_t cap = int64_t(256) * RK_PERSIST;
+        const dim3 grid(static_cast<uint32_t>(gr.count < cap ? gr.count : cap)), block(kStreamThreads);
+#else
         const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
+#endif
 #define RK_LAUNCH(XT, V)                                                                     \
     hipLaunchKernelGGL((rikfad_stream_kernel<XT, V>), grid, block, 0, stream, tensors, grads, \
-                       tiles, gr.begin, ws, k, pending)
+                       tiles, gr.begin, gr.count, ws, k, pending)
         if (gr.dtype == DT_F32) {
             if (gr.vec == 4) RK_LAUNCH(float, 4);
             else RK_LAUNCH(float, 1);

@@ -15,8 +15,11 @@ constexpr int kWave = 64;                       // CDNA wavefront
 constexpr int kThreads = 256;                   // workgroup of the small kernels
 constexpr int kStreamWaves = RK_STREAM_WAVES;   // waves per streaming workgroup
 constexpr int kStreamThreads = kWave * kStreamWaves;
-#ifndef RK_BATCH
-#define RK_BATCH 2
+#ifndef RK_RING_F32
+#define RK_RING_F32 3
+#endif
+#ifndef RK_RING_BF16
+#define RK_RING_BF16 2
 #endif
 #ifndef RK_BLOCK_LANES
 #define RK_BLOCK_LANES 64
@@ -24,7 +27,8 @@ constexpr int kStreamThreads = kWave * kStreamWaves;
 #ifndef RK_ROWS_PER_WAVE
 #define RK_ROWS_PER_WAVE 4
 #endif
-constexpr int kBatch = RK_BATCH;                // row loads in flight per wave
+constexpr int kRingF32 = RK_RING_F32;           // row loads in flight per wave (fp32)
+constexpr int kRingBF16 = RK_RING_BF16;         // the same for bf16 x/g
 constexpr int kMaxRowsPerWave = 64;             // lane t keeps row t's partial sum
 constexpr int kBlockLanes = RK_BLOCK_LANES;     // lanes per row of a full column block
 constexpr int kRowsPerWave = RK_ROWS_PER_WAVE;  // rows per wave of a matrix tile
@@ -33,7 +37,10 @@ constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kV
 
 enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 enum : int32_t { KIND_MATRIX = 0, KIND_VECTOR = 1 };
-enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1 };
+enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1, FIN_FOLD = 2 };
+
+constexpr int kSegStripes = 64;                 // stripes per column-sum segment
+constexpr int kFoldCols = 256;                  // columns per fold item
 
 // One parameter tensor.  Offsets are in floats into the context workspace.
 struct TensorDesc {
@@ -46,8 +53,9 @@ struct TensorDesc {
     int64_t rowpart;   // [ncb][m] row partial sums of [P^(1)]^2
     int64_t colpart;   // [nrs][n] column partial sums of [P^(1)]^2
     int64_t chunk;     // [nchunk] partial sums of R
+    int64_t colseg;    // [nseg][n] segment sums of the column partials (nseg > 1)
     int32_t nchunk, ncb, nrs, dtype;
-    int32_t kind, vec, pad0, pad1;
+    int32_t kind, vec, nseg, pad1;
 };
 
 // One workgroup of the streaming pass.
@@ -77,14 +85,19 @@ struct TileGroup {
     int64_t count;
 };
 
-// One workgroup of the finalisation pass.
+// One workgroup of the finalisation passes.
+//   FIN_ROWS  256 rows: R update and one partial sum of R.
+//   FIN_COLS  64 columns x one segment of up to kSegStripes stripes: a
+//             segment sum, or the C update when the tensor has one segment.
+//   FIN_FOLD  256 columns of a tensor with several segments: C update from
+//             the segment sums (second launch).
 struct FinItem {
     int32_t tensor;
-    int32_t kind;      // FIN_ROWS or FIN_COLS
+    int32_t kind;
     int32_t start;     // first row / column
-    int32_t count;     // rows (<= kChunkRows) / columns (<= 64)
-    int32_t chunk;     // FIN_ROWS: which partial sum of R this item writes
-    int32_t cwlog;     // FIN_COLS: log2 of columns per item (threads: cw x 256/cw)
+    int32_t count;     // rows / columns
+    int32_t chunk;     // FIN_ROWS: partial sum of R written; FIN_COLS: segment
+    int32_t pad;
 };
 
 // Step coefficients, computed in fp64 on the host and rounded once.

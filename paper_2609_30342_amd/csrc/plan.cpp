@@ -160,7 +160,7 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     const int32_t class_vec[5] = {4, 1, 8, 4, 1};
     std::vector<Tile> mat_tiles[5];
     std::vector<Tile> vec_tiles[2];
-    std::vector<FinItem> col_items;
+    std::vector<FinItem> col_items, fold_items;
     for (int64_t i = 0; i < count; ++i) {
         const rikfad_tensor &T = t[i];
         TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
@@ -258,15 +258,23 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                               static_cast<int32_t>(T.m - r0 < kChunkRows ? T.m - r0 : kChunkRows),
                               q, 0});
         }
-        // Column items: cw columns x 256/cw groups of stripes, with enough
-        // groups that each thread sums at most about 32 stripe partials.
-        int cwlog = 6;
-        while (cwlog > 2 && ceil_div(d.nrs, kThreads >> cwlog) > 32) --cwlog;
-        const int64_t cw = int64_t(1) << cwlog;
-        for (int64_t j0 = 0; j0 < T.n; j0 += cw)
-            col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
-                                 static_cast<int32_t>(T.n - j0 < cw ? T.n - j0 : cw), 0,
-                                 cwlog});
+        // Column items: 64 columns x one segment of kSegStripes stripes;
+        // tensors with several segments get fold items (second launch).
+        d.nseg = static_cast<int32_t>(ceil_div(d.nrs, kSegStripes));
+        if (d.nseg > 1) {
+            d.colseg = ws;
+            ws += round_up(int64_t(d.nseg) * T.n, 64);
+            for (int64_t j0 = 0; j0 < T.n; j0 += kFoldCols)
+                fold_items.push_back({static_cast<int32_t>(i), FIN_FOLD, static_cast<int32_t>(j0),
+                                      static_cast<int32_t>(T.n - j0 < kFoldCols ? T.n - j0
+                                                                                : kFoldCols),
+                                      0, 0});
+        }
+        for (int32_t q = 0; q < d.nseg; ++q)
+            for (int64_t j0 = 0; j0 < T.n; j0 += kWave)
+                col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
+                                     static_cast<int32_t>(T.n - j0 < kWave ? T.n - j0 : kWave), q,
+                                     0});
     }
     bool vec_placed[2] = {false, false};
     for (int cls = 0; cls < 5; ++cls) {
@@ -291,6 +299,8 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     }
     pl.row_items = static_cast<int64_t>(pl.fin.size());
     pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());
+    pl.fold_items = static_cast<int64_t>(fold_items.size());
+    pl.fin.insert(pl.fin.end(), fold_items.begin(), fold_items.end());
     pl.ws_floats = ws;
     if (pl.tiles.size() > static_cast<size_t>(INT32_MAX) || pl.fin.size() > static_cast<size_t>(INT32_MAX)) {
         err = "parameter set needs more than 2^31 workgroups";
