@@ -1,0 +1,270 @@
+// plan_check.cpp -- host-side check of the tile and finalisation tables.
+//
+// Builds random parameter lists, plans them with the library's own planner
+// and replays, on the CPU, the index arithmetic the gfx950 kernels perform
+// for every workgroup, wave and lane: every load and store address must lie
+// inside its buffer, every matrix and vector element must be updated
+// exactly once, every partial sum written exactly once and read only where
+// it was written, and the workspace regions must not overlap.  Built with
+// -fsanitize=address,undefined by the test that runs it.
+#include <cstdint>
+#include <cstdio>
+#include <random>
+#include <string>
+#include <vector>
+
+#include "../paper_2609_30342_amd/csrc/plan.hpp"
+
+using namespace rk;
+
+static int failures = 0;
+#define CHECK(cond, ...)                                            \
+    do {                                                            \
+        if (!(cond)) {                                              \
+            if (failures < 20) {                                    \
+                std::fprintf(stderr, "FAIL %s:%d: ", __FILE__, __LINE__); \
+                std::fprintf(stderr, __VA_ARGS__);                  \
+                std::fprintf(stderr, "\n");                         \
+            }                                                       \
+            ++failures;                                             \
+        }                                                           \
+    } while (0)
+
+struct Marks {
+    std::vector<uint8_t> v;
+    void init(int64_t n) { v.assign(static_cast<size_t>(n), 0); }
+    void hit(int64_t i, const char *what)
+    {
+        CHECK(i >= 0 && i < static_cast<int64_t>(v.size()), "%s index %lld out of [0,%zu)", what,
+              (long long)i, v.size());
+        if (i >= 0 && i < static_cast<int64_t>(v.size())) {
+            CHECK(v[static_cast<size_t>(i)] == 0, "%s index %lld written twice", what, (long long)i);
+            v[static_cast<size_t>(i)] = 1;
+        }
+    }
+    bool all() const
+    {
+        for (uint8_t b : v)
+            if (!b) return false;
+        return true;
+    }
+};
+
+static int ring_depth(int32_t dtype) { return dtype == DT_F32 ? kRingF32 : kRingBF16; }
+
+// Replays rikfad_stream_kernel's matrix-tile indexing.
+static void check_matrix_tile(const Plan &pl, const Tile &tl, std::vector<Marks> &elems,
+                              std::vector<Marks> &rowp, std::vector<Marks> &colp)
+{
+    const TensorDesc &td = pl.tensors[static_cast<size_t>(tl.tensor)];
+    const int64_t m = td.m, n = td.n, mn = m * n;
+    const int V = tl.vec, llog = tl.lanes_log2, L = 1 << llog, G = kWave >> llog;
+    const int B = ring_depth(tl.dtype);
+    CHECK(tl.rpw >= 1 && tl.rpw <= kMaxRowsPerWave, "rpw %d", tl.rpw);
+    CHECK(tl.ncols % V == 0 && tl.ncols <= L * V, "ncols %d L %d V %d", tl.ncols, L, V);
+    CHECK(tl.col0 % V == 0 && tl.col0 + tl.ncols <= n, "col range");
+    CHECK(tl.count <= kStreamWaves * tl.rpw && tl.start + tl.count <= m, "row range");
+    for (int wave = 0; wave < kStreamWaves; ++wave) {
+        const int64_t r0 = tl.start + int64_t(wave) * tl.rpw;
+        int nr = static_cast<int>(tl.start + tl.count - r0);
+        nr = nr < 0 ? 0 : (nr > tl.rpw ? tl.rpw : nr);
+        const int nld = (nr + G - 1) >> (6 - llog);
+        for (int lane = 0; lane < kWave; ++lane) {
+            const int seg = lane >> llog, sl = lane & (L - 1), ccol = sl * V;
+            const bool colok = ccol < tl.ncols;
+            const int64_t col = tl.col0 + ccol;
+            const int64_t lcol = colok ? col : tl.col0;
+            auto check_load = [&](int rl) {
+                const bool ok = colok && rl < nr;
+                const int64_t off = ok ? (r0 + rl) * n + lcol : r0 * n + lcol;
+                CHECK(off >= 0 && off + V <= mn && off % V == 0, "load off %lld mn %lld",
+                      (long long)off, (long long)mn);
+            };
+            if (nr > 0)
+                for (int u = 0; u < B; ++u) check_load(u * G + seg);
+            if (colok) CHECK(col + V <= n, "c load");
+            if (lane < nr) CHECK(r0 + lane < m, "r load");
+            for (int ld0 = 0; ld0 < nld; ld0 += B) {
+                for (int u = 0; u < B; ++u) {
+                    const int ld = ld0 + u, rl = ld * G + seg;
+                    if (colok && rl < nr) {
+                        for (int i = 0; i < V; ++i)
+                            elems[static_cast<size_t>(tl.tensor)].hit((r0 + rl) * n + col + i,
+                                                                      "element");
+                    }
+                    if (ld + B < nld) check_load((ld + B) * G + seg);
+                }
+            }
+            if (lane < nr)
+                rowp[static_cast<size_t>(tl.tensor)].hit(int64_t(tl.cb) * m + r0 + lane, "rowpart");
+        }
+    }
+    for (int j = 0; j < tl.ncols; ++j)
+        colp[static_cast<size_t>(tl.tensor)].hit(int64_t(tl.stripe) * n + tl.col0 + j, "colpart");
+}
+
+static void check_vector_tile(const Plan &pl, const Tile &tl, std::vector<Marks> &elems)
+{
+    const TensorDesc &td = pl.tensors[static_cast<size_t>(tl.tensor)];
+    const int64_t k = td.m * td.n;
+    CHECK(tl.start % tl.vec == 0 && tl.start + tl.count <= k, "vector tile range");
+    for (int64_t e = 0; e < tl.count; ++e)
+        elems[static_cast<size_t>(tl.tensor)].hit(tl.start + e, "vector element");
+}
+
+static void check_plan(const Plan &pl, int64_t count)
+{
+    std::vector<Marks> elems(static_cast<size_t>(count)), rowp(static_cast<size_t>(count)),
+        colp(static_cast<size_t>(count)), chunks(static_cast<size_t>(count)),
+        segcols(static_cast<size_t>(count)), folds(static_cast<size_t>(count)),
+        rows(static_cast<size_t>(count));
+    // workspace regions
+    std::vector<std::pair<int64_t, int64_t>> regions;
+    for (int64_t i = 0; i < count; ++i) {
+        const TensorDesc &td = pl.tensors[static_cast<size_t>(i)];
+        elems[static_cast<size_t>(i)].init(td.m * td.n);
+        if (td.kind == KIND_MATRIX) {
+            rowp[static_cast<size_t>(i)].init(int64_t(td.ncb) * td.m);
+            colp[static_cast<size_t>(i)].init(int64_t(td.nrs) * td.n);
+            chunks[static_cast<size_t>(i)].init(td.nchunk);
+            segcols[static_cast<size_t>(i)].init(int64_t(td.nseg) * td.n);
+            folds[static_cast<size_t>(i)].init(td.nseg > 1 ? td.n : 0);
+            rows[static_cast<size_t>(i)].init(td.m);
+            regions.push_back({td.rowpart, int64_t(td.ncb) * td.m});
+            regions.push_back({td.colpart, int64_t(td.nrs) * td.n});
+            regions.push_back({td.chunk, td.nchunk});
+            if (td.nseg > 1) regions.push_back({td.colseg, int64_t(td.nseg) * td.n});
+            CHECK(td.nseg == (td.nrs + kSegStripes - 1) / kSegStripes, "nseg");
+        }
+    }
+    for (size_t a = 0; a < regions.size(); ++a) {
+        CHECK(regions[a].first >= 0 && regions[a].first + regions[a].second <= pl.ws_floats,
+              "workspace region outside");
+        for (size_t b = a + 1; b < regions.size(); ++b) {
+            const bool disjoint = regions[a].first + regions[a].second <= regions[b].first ||
+                                  regions[b].first + regions[b].second <= regions[a].first;
+            CHECK(disjoint || regions[a].second == 0 || regions[b].second == 0, "regions overlap");
+        }
+    }
+    // groups partition the tile table; matrix tiles match their group class
+    int64_t covered = 0;
+    for (const TileGroup &g : pl.groups) {
+        CHECK(g.begin == covered, "groups not contiguous");
+        covered += g.count;
+        for (int64_t t = g.begin; t < g.begin + g.count; ++t) {
+            const Tile &tl = pl.tiles[static_cast<size_t>(t)];
+            CHECK(tl.dtype == g.dtype, "tile dtype vs group");
+            if (tl.kind == KIND_MATRIX) CHECK(tl.vec == g.vec, "tile vec vs group");
+        }
+    }
+    CHECK(covered == static_cast<int64_t>(pl.tiles.size()), "groups do not cover tiles");
+    for (const Tile &tl : pl.tiles) {
+        if (tl.kind == KIND_MATRIX) check_matrix_tile(pl, tl, elems, rowp, colp);
+        else check_vector_tile(pl, tl, elems);
+    }
+    // finalisation items
+    const int64_t nfin = static_cast<int64_t>(pl.fin.size());
+    for (int64_t q = 0; q < nfin; ++q) {
+        const FinItem &it = pl.fin[static_cast<size_t>(q)];
+        const TensorDesc &td = pl.tensors[static_cast<size_t>(it.tensor)];
+        CHECK(td.kind == KIND_MATRIX, "finalisation item on a vector");
+        if (it.kind == FIN_ROWS) {
+            CHECK(q < pl.row_items, "row item after the row range");
+            CHECK(it.count >= 1 && it.count <= kChunkRows, "row item count");
+            for (int t = 0; t < it.count; ++t) {
+                rows[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + t, "row item row");
+                for (int cb = 0; cb < td.ncb; ++cb)
+                    CHECK(int64_t(cb) * td.m + it.start + t < int64_t(td.ncb) * td.m, "rowpart read");
+            }
+            chunks[static_cast<size_t>(it.tensor)].hit(it.chunk, "chunk");
+        } else if (it.kind == FIN_COLS) {
+            CHECK(q >= pl.row_items && q < nfin - pl.fold_items, "column item placement");
+            CHECK(it.count >= 1 && it.count <= kWave && it.chunk < td.nseg, "column item");
+            for (int j = 0; j < it.count; ++j) {
+                segcols[static_cast<size_t>(it.tensor)].hit(int64_t(it.chunk) * td.n + it.start + j,
+                                                             "segment column");
+                const int seg0 = it.chunk * kSegStripes;
+                for (int w = 0; w < 4; ++w) {
+                    const int s0 = std::min(td.nrs, seg0 + w * (kSegStripes / 4));
+                    const int s1 = std::min(td.nrs, s0 + kSegStripes / 4);
+                    for (int s = s0; s < s1; ++s)
+                        CHECK(int64_t(s) * td.n + it.start + j < int64_t(td.nrs) * td.n,
+                              "colpart read");
+                }
+            }
+        } else {
+            CHECK(it.kind == FIN_FOLD && q >= nfin - pl.fold_items, "fold item placement");
+            CHECK(td.nseg > 1 && it.count >= 1 && it.count <= kFoldCols, "fold item");
+            for (int t = 0; t < it.count; ++t)
+                folds[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + t, "fold column");
+        }
+    }
+    for (int64_t i = 0; i < count; ++i) {
+        const TensorDesc &td = pl.tensors[static_cast<size_t>(i)];
+        CHECK(elems[static_cast<size_t>(i)].all(), "tensor %lld (%lldx%lld) not fully covered",
+              (long long)i, (long long)td.m, (long long)td.n);
+        if (td.kind == KIND_MATRIX) {
+            CHECK(rowp[static_cast<size_t>(i)].all(), "row partials incomplete");
+            CHECK(colp[static_cast<size_t>(i)].all(), "column partials incomplete");
+            CHECK(chunks[static_cast<size_t>(i)].all(), "chunks incomplete");
+            CHECK(rows[static_cast<size_t>(i)].all(), "row items incomplete");
+            CHECK(segcols[static_cast<size_t>(i)].all(), "segment columns incomplete");
+            CHECK(folds[static_cast<size_t>(i)].all(), "fold columns incomplete");
+        }
+    }
+}
+
+int main(int argc, char **argv)
+{
+    const int trials = argc > 1 ? std::atoi(argv[1]) : 300;
+    std::mt19937_64 rng(12345);
+    const int64_t dims[] = {1, 2, 3, 4, 5, 7, 8, 12, 16, 27, 31, 33, 63, 64, 65, 100, 127, 128,
+                            129, 255, 256, 257, 300, 384, 513, 640, 768, 776, 1000, 1024, 1152,
+                            1440, 2304, 3072, 4097};
+    const int ndims = sizeof(dims) / sizeof(dims[0]);
+    const uintptr_t base = uintptr_t(1) << 40;
+    int planned = 0, rejected = 0;
+    for (int trial = 0; trial < trials; ++trial) {
+        const int count = static_cast<int>(rng() % 9);
+        std::vector<rikfad_tensor> ts(static_cast<size_t>(count));
+        bool expect_align_error = false;
+        for (int i = 0; i < count; ++i) {
+            rikfad_tensor &t = ts[static_cast<size_t>(i)];
+            t.m = dims[rng() % ndims];
+            t.n = dims[rng() % ndims];
+            if (rng() % 40 == 0) t.m = 50257;
+            t.dtype = (rng() % 2) ? RIKFAD_BF16 : RIKFAD_FP32;
+            t.reserved = 0;
+            const uintptr_t slot = base + (uintptr_t(i) << 34);
+            const int es = t.dtype == RIKFAD_BF16 ? 2 : 4;
+            // mostly aligned buffers, sometimes element-aligned views
+            const uintptr_t offx = (rng() % 5 == 0) ? uintptr_t(es) * (rng() % 4) : 0;
+            const uintptr_t offg = (rng() % 5 == 0) ? uintptr_t(es) * (rng() % 4) : 0;
+            const uintptr_t offp = (rng() % 7 == 0) ? 4 * (rng() % 4) : 0;
+            t.x = reinterpret_cast<void *>(slot + offx);
+            t.g = reinterpret_cast<const void *>(slot + (uintptr_t(1) << 32) + offg);
+            t.p = reinterpret_cast<float *>(slot + (uintptr_t(2) << 32) + offp);
+            t.r = reinterpret_cast<float *>(slot + (uintptr_t(3) << 32));
+            t.c = reinterpret_cast<float *>(slot + (uintptr_t(3) << 32) + (uintptr_t(1) << 31));
+            if (rng() % 50 == 0) {      // a misaligned pointer must be rejected
+                t.p = reinterpret_cast<float *>(reinterpret_cast<uintptr_t>(t.p) + 2);
+                expect_align_error = true;
+            }
+        }
+        Plan pl;
+        std::string err;
+        const rikfad_status s = plan_rikfad(ts.data(), count, pl, err);
+        if (expect_align_error) {
+            CHECK(s == RIKFAD_EALIGN, "misaligned p accepted (status %d)", s);
+            ++rejected;
+            continue;
+        }
+        CHECK(s == RIKFAD_OK, "plan failed: %s", err.c_str());
+        if (s != RIKFAD_OK) continue;
+        ++planned;
+        check_plan(pl, count);
+    }
+    std::printf("plan_check: %d plans checked, %d rejected as expected, %d failures\n", planned,
+                rejected, failures);
+    return failures == 0 ? 0 : 1;
+}
