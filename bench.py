@@ -154,6 +154,26 @@ def time_small(specs, hp, steps, warmup, seed=0):
             "graph_params_per_s": n / (graph * 1e-3)}
 
 
+def time_friction_report(m, n, iters=30, reps=3):
+    """Rank-1 friction diagnostic on an m x n friction tensor: ms per call and
+    GB/s on the passes over xi it makes (3 + 2 iters + 1 reads of 4 m n)."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    gen = torch.Generator(device="cuda:0").manual_seed(7)
+    xi = torch.rand((m, n), generator=gen, device="cuda:0")
+    s = torch.cuda.current_stream().cuda_stream
+    R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s)
+    ms = (time.perf_counter() - t0) / reps * 1e3
+    passes = 3 + 2 * iters + 1
+    del xi
+    torch.cuda.empty_cache()
+    return {"shape": [m, n], "power_iters": iters, "ms": ms,
+            "gbps": passes * 4.0 * m * n / (ms * 1e-3) / 1e9}
+
+
 def time_probe(nfloat, reps=10):
     """3-read / 2-write fp32 stream of the same byte count as the step."""
     import torch
@@ -296,6 +316,7 @@ def main():
                                       "hbm_gbps": 28.0 * N / (ik_ms * 1e-3) / 1e9,
                                       "state_bytes": info["ikfad_state_bytes"]}
         var["probe_3r2w_gbps"] = time_probe(N)
+        var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {
             "single_256x512_fp32": time_small(synth.single_matrix(), hp, 200, 5),
             "gpt2_nano_fp32": time_small(synth.gpt2_nano(), hp, 100, 5),

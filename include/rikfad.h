@@ -221,6 +221,37 @@ rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps);
 void ikfad_destroy(ikfad_ctx *ctx);
 
 /* ------------------------------------------------------------------------
+ * Rank-1 friction diagnostic (Section 4, "How close is xi~ to the best
+ * rank-1 friction?").  The paper runs iKFAD0 and carries R-iKFAD's factors
+ * as shadow states fed by the same P^(1); since both obey the same linear
+ * filter, from zero they are exactly R = xi 1 and C = xi^T 1.  Given an
+ * iKFAD friction tensor xi (m x n fp32, row-major, device memory, e.g. the
+ * xi of an ikfad context), this computes on the GPU the shadow factors,
+ * |xi|_F^2, |xi - xi~|_F^2 with xi~ = R C^T / (1^T R + eps_stab), and the
+ * leading singular value sigma_1 of xi by power_iters steps of power
+ * iteration on xi^T xi from C / |C|; then the relative error, the
+ * Eckart-Young floor sqrt(1 - sigma_1^2 / |xi|_F^2) and the stable rank
+ * |xi|_F^2 / sigma_1^2.  All reductions are fp64 in a fixed order.
+ * Blocking (waits for `stream`); allocates and frees a temporary device
+ * workspace of about 8 (2 m + 2 n + n m / 64) bytes.  m < 4,194,240.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    double xi_fro2;            /* |xi|_F^2 */
+    double err_fro2;           /* |xi - xi~|_F^2 */
+    double sum_r;              /* 1^T R = 1^T xi 1 */
+    double sigma1;             /* leading singular value of xi */
+    double rel_err;            /* |xi - xi~|_F / |xi|_F */
+    double eckart_young_floor; /* best possible rank-1 relative error */
+    double stable_rank;        /* |xi|_F^2 / sigma_1^2 */
+    int32_t power_iters;
+    int32_t reserved;
+} rikfad_friction_stats;
+
+rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n, double eps_stab,
+                                     int32_t power_iters, void *stream,
+                                     rikfad_friction_stats *out);
+
+/* ------------------------------------------------------------------------
  * Bandwidth probes (measurement aids for the HBM roofline).
  *   rikfad_probe_stream: d[i] = a[i] + b[i], e[i] = a[i] * c[i] over nfloat
  *     fp32 elements -- the 3-read / 2-write mix of the fp32 step, with no

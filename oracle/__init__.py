@@ -204,3 +204,28 @@ def quadratic_run(A, x, p, r, c, hp: HParams, nsteps, every):
                                    int(nsteps), int(every), energy.ctypes.data,
                                    ctypes.byref(worst)), "quadratic_run")
     return energy, worst.value
+
+
+def friction_report(xi, eps_stab):
+    """Rank-1 friction statistics of a full iKFAD friction tensor (Section 4,
+    "How Close is xi~ to the Best Rank-1 Friction?"), from their definitions:
+    shadow factors R = xi 1 and C = xi^T 1 (the R-iKFAD filter fed by the
+    same P^(1), started at zero, is linear and equals these sums), rank-1
+    friction xi~ = R C^T / (1^T R + eps_stab) (0 if the denominator is 0),
+    relative error |xi - xi~|_F / |xi|_F, leading singular value sigma_1
+    from numpy's SVD, Eckart-Young floor sqrt(1 - sigma_1^2 / |xi|_F^2) and
+    stable rank |xi|_F^2 / sigma_1^2.  fp64."""
+    xi = np.asarray(xi, dtype=np.float64)
+    r = xi.sum(axis=1)
+    c = xi.sum(axis=0)
+    s = r.sum()
+    denom = s + eps_stab
+    xit = np.outer(r, c) / denom if denom != 0.0 else np.zeros_like(xi)
+    fro2 = float(np.sum(xi * xi))
+    err2 = float(np.sum((xi - xit) ** 2))
+    sigma1 = float(np.linalg.svd(xi, compute_uv=False)[0])
+    ratio = sigma1 ** 2 / fro2 if fro2 > 0 else 1.0
+    return {"xi_fro2": fro2, "err_fro2": err2, "sum_r": float(s), "sigma1": sigma1,
+            "rel_err": float(np.sqrt(err2 / fro2)) if fro2 > 0 else 0.0,
+            "eckart_young_floor": float(np.sqrt(max(0.0, 1.0 - ratio))),
+            "stable_rank": fro2 / sigma1 ** 2 if sigma1 > 0 else 0.0}

@@ -30,9 +30,10 @@ def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     hipcc = os.path.join(ROCM, "bin", "hipcc")
     objs = []
-    o = os.path.join(BUILD, "kernels.o")
-    _run([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "kernels.hip"), "-o", o], verbose)
-    objs.append(o)
+    for src in ("kernels.hip", "diag.hip"):
+        o = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        objs.append(o)
     for src in ("plan.cpp", "api.cpp"):
         o = os.path.join(BUILD, src.replace(".cpp", ".o"))
         _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", o], verbose)

@@ -53,6 +53,12 @@ class rikfad_info(ctypes.Structure):
         "finalize_items")] + [("pending", ctypes.c_int32), ("two_pass", ctypes.c_int32)]
 
 
+class rikfad_friction_stats(ctypes.Structure):
+    _fields_ = [(nm, ctypes.c_double) for nm in (
+        "xi_fro2", "err_fro2", "sum_r", "sigma1", "rel_err", "eckart_young_floor",
+        "stable_rank")] + [("power_iters", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 _lib = None
 
 # name -> (restype, argtypes)
@@ -81,6 +87,8 @@ _SIGNATURES = {
     "ikfad_timing_enable": (_st, [_vp, _i32]),
     "ikfad_timing_read": (_st, [_vp, _P(ctypes.c_double), _P(_i64)]),
     "ikfad_destroy": (None, [_vp]),
+    "rikfad_friction_report": (_st, [_vp, _i64, _i64, ctypes.c_double, _i32, _vp,
+                                     _P(rikfad_friction_stats)]),
     "rikfad_probe_stream": (_st, [_vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "rikfad_probe_copy": (_st, [_vp, _vp, _i64, _vp]),
 }
@@ -221,6 +229,15 @@ def ikfad_timing_read(ctx):
 def ikfad_destroy(ctx):
     if ctx:
         lib().ikfad_destroy(ctx)
+
+
+def rikfad_friction_report(xi, m, n, eps_stab=0.0, power_iters=60, stream=None):
+    """Rank-1 friction statistics of an iKFAD friction tensor (device
+    pointer, m x n fp32); blocking.  Returns a dict."""
+    out = rikfad_friction_stats()
+    _check(lib().rikfad_friction_report(xi, int(m), int(n), float(eps_stab), int(power_iters),
+                                        stream, ctypes.byref(out)), "rikfad_friction_report")
+    return {nm: getattr(out, nm) for nm, _ in rikfad_friction_stats._fields_}
 
 
 def rikfad_probe_stream(a, b, c, d, e, nfloat, stream=None):

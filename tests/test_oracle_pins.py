@@ -428,3 +428,54 @@ def test_quadratic_positive_damping_is_exponential():
     corr = np.corrcoef(t[sel], np.log(E[sel]))[0, 1]
     assert slope < -0.2 and corr < -0.999
     assert worst <= 1e-12
+
+
+# ------------------------------------- rank-1 friction diagnostic (Section 4)
+
+def test_friction_report_rank1_tensor_is_exact():
+    """A rank-1 non-negative friction a b^T: shadow factors R = a sum(b),
+    C = b sum(a), so at eps = 0 xi~ reproduces it exactly; sigma_1 =
+    |a| |b|, floor 0, stable rank 1 (closed forms)."""
+    rng = _rng(30)
+    a, b = rng.random(17), rng.random(23)
+    rep = O.friction_report(np.outer(a, b), 0.0)
+    assert rep["rel_err"] < 1e-14 and rep["eckart_young_floor"] < 1e-7
+    assert rep["sigma1"] == pytest.approx(np.linalg.norm(a) * np.linalg.norm(b), rel=1e-14)
+    assert rep["stable_rank"] == pytest.approx(1.0, rel=1e-13)
+    assert rep["sum_r"] == pytest.approx(a.sum() * b.sum(), rel=1e-14)
+
+
+def test_friction_report_floor_is_best_rank1_error():
+    """Eckart-Young: no rank-1 matrix is closer to xi than the truncated SVD,
+    whose relative error is sqrt(1 - sigma_1^2 / |xi|_F^2); the rank-1
+    friction can never beat it."""
+    rng = _rng(31)
+    xi = sum(np.outer(rng.random(40), rng.random(30)) for _ in range(3)) + 0.05 * rng.random((40, 30))
+    rep = O.friction_report(xi, 1e-8)
+    U, S, Vt = np.linalg.svd(xi)
+    best = np.linalg.norm(xi - S[0] * np.outer(U[:, 0], Vt[0])) / np.linalg.norm(xi)
+    assert rep["eckart_young_floor"] == pytest.approx(best, rel=1e-10)
+    assert rep["rel_err"] >= rep["eckart_young_floor"] - 1e-12
+    assert 1.0 < rep["stable_rank"] < 3.0
+
+
+def test_shadow_factors_are_row_and_column_sums_of_xi():
+    """Section 4 carries R-iKFAD's factors as shadows of an iKFAD run: R and C
+    follow R' = a R + kappa [P^(1)]^2 1 while xi' = a xi + kappa [P^(1)]^2,
+    so from zero R = xi 1 and C = xi^T 1 at every step.  Checked along an
+    oracle iKFAD trajectory, reading P^(1) back from the friction update."""
+    rng = _rng(32)
+    m, n = 12, 9
+    hp = O.HParams(h=0.1, gamma=0.0, alpha=0.3, mu=0.1, eps_stab=1e-8)
+    a, kappa, _ = O.coefficients(hp)
+    x, p, xi = rng.standard_normal(m * n) * 0.02, np.zeros(m * n), np.zeros(m * n)
+    R, C = np.zeros(m), np.zeros(n)
+    for _ in range(15):
+        xi_old = xi.copy()
+        O.ikfad_step(x, rng.standard_normal(m * n), p, xi, hp)
+        p1sq = ((xi - a * xi_old) / kappa).reshape(m, n)
+        R = a * R + kappa * p1sq.sum(axis=1)
+        C = a * C + kappa * p1sq.sum(axis=0)
+        X = xi.reshape(m, n)
+        np.testing.assert_allclose(R, X.sum(axis=1), rtol=1e-10)
+        np.testing.assert_allclose(C, X.sum(axis=0), rtol=1e-10)
