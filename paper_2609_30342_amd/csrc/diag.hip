@@ -10,7 +10,7 @@
 // exactly R = xi 1 and C = xi^T 1: this file computes them from xi directly.
 //
 // Every quantity is a deterministic reduction (fixed partition, fixed
-// order): row sums one wave per row, column sums in 256-row stripes then
+// order): row sums one wave per row, column sums in row stripes then
 // folded in stripe order, squared norms per workgroup then folded in order.
 // sigma_1 comes from power iteration on xi^T xi started at C / |C| (xi >= 0,
 // so the leading singular vectors are non-negative), normalised on the GPU.
@@ -24,7 +24,6 @@
 namespace {
 
 constexpr int kT = 256;            // threads per workgroup
-constexpr int kStripe = 256;       // rows per column-sum stripe
 constexpr int kStatChunk = 4096;   // elements per workgroup of the vector statistics
 constexpr int kErrRows = 16;       // rows per workgroup of the error pass
 
@@ -69,14 +68,15 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
 
 // part[s, j] = sum over rows i of stripe s of xi[i, j] * (w ? w[i] : 1).
 __global__ __launch_bounds__(kT) void col_partial_kernel(const float *__restrict__ xi, int64_t m,
-                                                         int64_t n, const double *__restrict__ w,
+                                                         int64_t n, int64_t stripe,
+                                                         const double *__restrict__ w,
                                                          double *__restrict__ part)
 {
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kT + threadIdx.x;
     const int64_t s = blockIdx.y;
     if (j >= n) return;
-    const int64_t i0 = s * kStripe;
-    const int64_t i1 = i0 + kStripe < m ? i0 + kStripe : m;
+    const int64_t i0 = s * stripe;
+    const int64_t i1 = i0 + stripe < m ? i0 + stripe : m;
     double acc = 0.0;
     // Sixteen rows in flight per thread; additions in row order.
     for (int64_t ib = i0; ib < i1; ib += 16) {
@@ -236,8 +236,14 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
         return RIKFAD_EINVAL;
     if (reinterpret_cast<uintptr_t>(xi) % 4 != 0) return RIKFAD_EALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream_);
-    const int64_t nstripes = (m + kStripe - 1) / kStripe;
-    if (nstripes > 65535) return RIKFAD_EINVAL;      // grid y limit
+    // Stripe height: the largest power of two in [16, 1024] that still gives
+    // the column pass about eight workgroups per compute unit, raised if the
+    // stripe count would pass the grid's y limit.
+    const int64_t ncb = (n + kT - 1) / kT;
+    int64_t stripe = 1024;
+    while (stripe > 16 && ncb * ((m + stripe - 1) / stripe) < 2048) stripe >>= 1;
+    while ((m + stripe - 1) / stripe > 65535) stripe <<= 1;
+    const int64_t nstripes = (m + stripe - 1) / stripe;
     const int64_t nerr = (m + kErrRows - 1) / kErrRows;
     const int64_t mk = m > n ? m : n;
     const int64_t nstat = (mk + kStatChunk - 1) / kStatChunk;
@@ -252,7 +258,7 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     double *stats_r = spart + 2 * nstat, *stats_v = stats_r + 2, *stats_u = stats_v + 2;
     double *err = stats_u + 2, *scale_v = err + 2;
     const dim3 rows_grid(static_cast<uint32_t>((m + kT / 64 - 1) / (kT / 64)));
-    const dim3 cols_grid(static_cast<uint32_t>((n + kT - 1) / kT), static_cast<uint32_t>(nstripes));
+    const dim3 cols_grid(static_cast<uint32_t>(ncb), static_cast<uint32_t>(nstripes));
     const dim3 fold_grid(static_cast<uint32_t>((n + kT - 1) / kT));
     auto stats = [&](const double *vec, int64_t k, double *res, double *scale) {
         const int64_t nc = (k + kStatChunk - 1) / kStatChunk;
@@ -263,7 +269,8 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
 
     // Shadow factors R = xi 1, C = xi^T 1 and their totals.
     hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, nullptr, nullptr, r);
-    hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, nullptr, cpart);
+    hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, nullptr,
+                       cpart);
     hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, nullptr, c);
     stats(r, m, stats_r, nullptr);
     // |xi|_F^2 and |xi - xi~|_F^2
@@ -275,7 +282,8 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     const double *vin = c;
     for (int it = 0; it < power_iters; ++it) {
         hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, scale_v, u);
-        hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, u, cpart);
+        hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, u,
+                           cpart);
         hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes,
                            nullptr, v);
         stats(v, n, stats_v, scale_v);
