@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE.  Only the test suite, ``__graft_entry__.smoke()`` and
 the CPU-baseline leg of ``bench.py`` may import this module.  It wraps the
 plain C implementation in ``rikfad_oracle.c`` (built by ``oracle.build``),
 which follows the paper's App. A Table of sub-step updates literally in
-fp64.  It shares no code with the GPU package and never imports it.
+fp64, and ``adafm_oracle.c``, the paper's Adafactor-m baseline step.  It shares no code with the GPU package and never imports it.
 """
 from __future__ import annotations
 
@@ -24,6 +24,13 @@ class _HP(ctypes.Structure):
     _fields_ = [("h", ctypes.c_double), ("gamma", ctypes.c_double),
                 ("alpha", ctypes.c_double), ("mu", ctypes.c_double),
                 ("eps_stab", ctypes.c_double)]
+
+
+class _AdaHP(ctypes.Structure):
+    _fields_ = [("h", ctypes.c_double), ("beta1", ctypes.c_double),
+                ("decay_rate", ctypes.c_double), ("eps1", ctypes.c_double),
+                ("eps2", ctypes.c_double), ("clip_threshold", ctypes.c_double),
+                ("scale_parameter", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class _Tensor(ctypes.Structure):
@@ -54,8 +61,15 @@ def lib():
         L.orc_round_bf16_array.restype = None
         L.orc_quadratic_run.argtypes = [i64, i64, vp, vp, vp, vp, vp, hp, i64, i64,
                                         vp, vp]
+        ahp = ctypes.POINTER(_AdaHP)
+        L.orc_adafm_beta2.argtypes = [i64, ctypes.c_double]
+        L.orc_adafm_beta2.restype = ctypes.c_double
+        L.orc_adafm_matrix_step.argtypes = [i64, i64, i64, i32, vp, vp, vp, vp, vp, vp, ahp]
+        L.orc_adafm_vector_step.argtypes = [i64, i64, i32, vp, vp, vp, vp, vp, ahp]
+        L.orc_adafm_step_list.argtypes = [i64, vp, i64, ahp, ctypes.c_int]
         for fn in (L.orc_coefficients, L.orc_rank1_friction, L.orc_rikfad_matrix_step,
-                   L.orc_ikfad_step, L.orc_rikfad_step_list, L.orc_quadratic_run):
+                   L.orc_ikfad_step, L.orc_rikfad_step_list, L.orc_quadratic_run,
+                   L.orc_adafm_matrix_step, L.orc_adafm_vector_step, L.orc_adafm_step_list):
             fn.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -229,3 +243,73 @@ def friction_report(xi, eps_stab):
             "rel_err": float(np.sqrt(err2 / fro2)) if fro2 > 0 else 0.0,
             "eckart_young_floor": float(np.sqrt(max(0.0, 1.0 - ratio))),
             "stable_rank": fro2 / sigma1 ** 2 if sigma1 > 0 else 0.0}
+
+
+# ------------------------------------------------------------- Adafactor-m
+
+@dataclass
+class AdafmHParams:
+    """Adafactor-m hyperparameters: step size h, first-moment decay beta1,
+    second-moment schedule beta2_t = 1 - t^decay_rate, eps1 added to G^2,
+    eps2 floor of RMS(X) for the optional parameter scale, update clipping
+    threshold (<= 0: off)."""
+    h: float
+    beta1: float = 0.9
+    decay_rate: float = -0.8
+    eps1: float = 1e-30
+    eps2: float = 1e-3
+    clip_threshold: float = 1.0
+    scale_parameter: bool = False
+
+    def _c(self):
+        return _AdaHP(self.h, self.beta1, self.decay_rate, self.eps1, self.eps2,
+                      self.clip_threshold, int(bool(self.scale_parameter)), 0)
+
+
+def adafm_beta2(t, decay_rate=-0.8):
+    """Second-moment decay of step t: 1 - t^decay_rate."""
+    return lib().orc_adafm_beta2(int(t), float(decay_rate))
+
+
+def adafm_matrix_step(x, g, mom, r, c, t, hp: AdafmHParams, x_bf16=False, x_unrounded=None):
+    """Adafactor-m step t on an m x n matrix; x, mom, r, c updated in place."""
+    m, n = x.shape
+    for nm, a in (("x", x), ("mom", mom), ("r", r), ("c", c)):
+        _need_f64(nm, a)
+    g = _f64(g)
+    if x_unrounded is not None:
+        _need_f64("x_unrounded", x_unrounded)
+    _check(lib().orc_adafm_matrix_step(m, n, int(t), int(bool(x_bf16)), x.ctypes.data,
+                                       _ptr(x_unrounded), g.ctypes.data, mom.ctypes.data,
+                                       r.ctypes.data, c.ctypes.data, ctypes.byref(hp._c())),
+           "adafm matrix step")
+
+
+def adafm_vector_step(x, g, mom, v, t, hp: AdafmHParams, x_bf16=False, x_unrounded=None):
+    """Adafactor-m step t on a non-2D parameter (unfactored second moment v)."""
+    for nm, a in (("x", x), ("mom", mom), ("v", v)):
+        _need_f64(nm, a)
+    g = _f64(g)
+    if x_unrounded is not None:
+        _need_f64("x_unrounded", x_unrounded)
+    _check(lib().orc_adafm_vector_step(x.size, int(t), int(bool(x_bf16)), x.ctypes.data,
+                                       _ptr(x_unrounded), g.ctypes.data, mom.ctypes.data,
+                                       v.ctypes.data, ctypes.byref(hp._c())),
+           "adafm vector step")
+
+
+def adafm_step_list(tensors, grads, t, hp: AdafmHParams, threads=1):
+    """Adafactor-m step t over a list of OracleTensor (p = first moment; a
+    vector keeps its second moment in ``xi``)."""
+    arr = (_Tensor * max(1, len(tensors)))()
+    keep = []
+    for i, (T, g) in enumerate(zip(tensors, grads)):
+        g = _f64(g)
+        if g.size != T.m * T.n:
+            raise ValueError("gradient size mismatch")
+        keep.append(g)
+        arr[i] = _Tensor(T.x.ctypes.data, _ptr(T.x_unrounded), g.ctypes.data,
+                         T.p.ctypes.data, T.r.ctypes.data, T.c.ctypes.data,
+                         T.m, T.n, int(T.bf16), 0)
+    _check(lib().orc_adafm_step_list(len(tensors), ctypes.addressof(arr), int(t),
+                                     ctypes.byref(hp._c()), int(threads)), "adafm step_list")
