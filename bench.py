@@ -30,7 +30,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "stream_kernel_gpt2s_traffic.json"
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for nm in ("kernels.hip", "layout.hpp", "plan.cpp"):
+    for nm in ("kernels.hip", "device.hpp", "layout.hpp", "plan.cpp"):
         with open(os.path.join(ROOT, "paper_2609_30342_amd", "csrc", nm), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -116,6 +116,39 @@ def time_ikfad(specs, hp, steps, warmup, seed=0):
     del xs, gs
     torch.cuda.empty_cache()
     return ms / n
+
+
+def time_adafm(specs, dtype, steps, warmup, seed=0, **hp):
+    """Adafactor-m (the paper's baseline) on the same parameter set: whole
+    step time and the library's per-pass event timing."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    xs, gs = build_workload(specs, dtype, seed, torch.device("cuda:0"))
+    opt = R.ADAFM(xs, gs, **hp)
+    total, upd_bytes, state = R.adafm_min_bytes(opt.ctx)
+    for _ in range(warmup):
+        opt.step()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        opt.step()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    R.adafm_timing_enable(opt.ctx, True)
+    for _ in range(steps):
+        opt.step()
+    (stats, fin, rms, upd), n = R.adafm_timing_read(opt.ctx)
+    opt.close()
+    del xs, gs
+    torch.cuda.empty_cache()
+    return {"ms_per_step": ms, "params_per_s": sum(s.numel for s in specs) / (ms * 1e-3),
+            "hbm_gbps_step": total / (ms * 1e-3) / 1e9, "min_bytes_per_step": total,
+            "state_bytes": state,
+            "pass_ms": {"stats": stats / n, "finalize": fin / n, "rms_scale": rms / n,
+                        "update": upd / n},
+            "update_gbps": upd_bytes / (upd / n * 1e-3) / 1e9}
 
 
 def time_small(specs, hp, steps, warmup, seed=0):
@@ -315,6 +348,10 @@ def main():
             var["ikfad_full_fp32"] = {"ms_per_step": ik_ms, "params_per_s": N / (ik_ms * 1e-3),
                                       "hbm_gbps": 28.0 * N / (ik_ms * 1e-3) / 1e9,
                                       "state_bytes": info["ikfad_state_bytes"]}
+        var["adafm_fp32"] = time_adafm(synth.gpt2_small("fp32"), "fp32", args.steps,
+                                       args.warmup, h=1e-3, beta1=0.9)
+        var["adafm_bf16"] = time_adafm(synth.gpt2_small("bf16"), "bf16", args.steps,
+                                       args.warmup, h=1e-3, beta1=0.9)
         var["probe_3r2w_gbps"] = time_probe(N)
         var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {

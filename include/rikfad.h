@@ -233,7 +233,10 @@ void ikfad_destroy(ikfad_ctx *ctx);
  * Eckart-Young floor sqrt(1 - sigma_1^2 / |xi|_F^2) and the stable rank
  * |xi|_F^2 / sigma_1^2.  All reductions are fp64 in a fixed order.
  * Blocking (waits for `stream`); allocates and frees a temporary device
- * workspace of about 8 (2 m + 2 n + n m / 64) bytes.  m < 4,194,240.
+ * workspace of 8 (2 m + 2 n + n ceil(m / s)) bytes plus a little, where the
+ * column-sum stripe height s is a power of two in [16, 1024] (larger only
+ * for m above 2^20).  m, n < 2^31; EINVAL on bad arguments, ENOMEM if the
+ * workspace cannot be allocated, EHIP on a launch or copy failure.
  * ---------------------------------------------------------------------- */
 typedef struct {
     double xi_fro2;            /* |xi|_F^2 */
@@ -250,6 +253,67 @@ typedef struct {
 rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n, double eps_stab,
                                      int32_t power_iters, void *stream,
                                      rikfad_friction_stats *out);
+
+/* ------------------------------------------------------------------------
+ * Adafactor-m (the paper's baseline optimiser; Section 2, Methodology,
+ * left-hand system, and eq. (xi_def) for zeta^ = R C^T / 1^T R).  The
+ * second moment of the gradient is factored as R (row sums) and C (column
+ * sums), the first moment M is kept in full, and the factors act in the
+ * position equation.  Discrete step t (t = 1, 2, ...; Section 3 and App.
+ * "Hyperparameters": beta2_t = 1 - t^{-0.8}, no relative step, no warm-up),
+ * the factored algorithm of Shazeer & Stern (2018) with update clipping:
+ *   b = 1 - t^decay_rate;  Q = G^2 + eps1
+ *   R <- b R + (1-b) Q 1_n;  C <- b C + (1-b) Q^T 1_m
+ *   U = G / sqrt(R C^T / 1^T R)               (U = 0 where that is 0)
+ *   s = h * (scale_parameter ? max(eps2, RMS(X)) : 1) / max(1, RMS(U) / d)
+ *       (no clipping when d = clip_threshold <= 0; RMS = root mean square
+ *        over the tensor, X before the step)
+ *   M <- beta1 M + (1 - beta1) s U;  X <- X - M (bf16 x: rounded to nearest even)
+ * Vectors (m == 1 or n == 1) keep the unfactored second moment v (m*n fp32,
+ * in c when m == 1, else in r) and use U = G / sqrt(v).
+ *
+ * Tensors reuse rikfad_tensor: p is the first moment M (m*n fp32), r and c
+ * the factors (zero-filled by the caller before the first step).  The
+ * caller owns every buffer; the context owns its tables and workspace.
+ * Three passes stream the gradient (statistics, RMS of U, update), so a
+ * step moves 28 bytes per fp32 parameter (18 with bf16 x and g; +4 / +2
+ * with scale_parameter).  Every call enqueues on `stream` and returns;
+ * same error conventions as the R-iKFAD entry points.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    double h;                /* step size (learning rate), > 0 */
+    double beta1;            /* first-moment decay, 0 <= beta1 < 1 */
+    double decay_rate;       /* beta2_t = 1 - t^decay_rate, <= 0 (paper: -0.8) */
+    double eps1;             /* added to G^2, >= 0 (1e-30) */
+    double eps2;             /* floor of RMS(X) in the parameter scale, >= 0 (1e-3) */
+    double clip_threshold;   /* update clipping d, <= 0 disables it (1.0) */
+    int32_t scale_parameter; /* 0 or 1 */
+    int32_t reserved;        /* must be 0 */
+} adafm_hparams;
+
+typedef struct adafm_ctx adafm_ctx;
+
+/* Validates like rikfad_create; the step counter starts at 0. */
+rikfad_status adafm_create(const rikfad_tensor *tensors, int64_t count,
+                           const adafm_hparams *hp, adafm_ctx **out);
+/* Enqueues step t = (steps taken) + 1. */
+rikfad_status adafm_step(adafm_ctx *ctx, void *stream);
+/* As adafm_step with new gradient pointers (same rules as rikfad_step_grads). */
+rikfad_status adafm_step_grads(adafm_ctx *ctx, const void *const *grads, void *stream);
+rikfad_status adafm_set_hparams(adafm_ctx *ctx, const adafm_hparams *hp);
+/* Steps taken so far (for resuming from a checkpoint), >= 0. */
+rikfad_status adafm_set_step(adafm_ctx *ctx, int64_t steps_taken);
+rikfad_status adafm_get_step(const adafm_ctx *ctx, int64_t *steps_taken);
+/* Bytes the step must move (read x, g, M and g twice; write x, M; R, C). */
+rikfad_status adafm_min_bytes(const adafm_ctx *ctx, int64_t *min_bytes_per_step,
+                              int64_t *update_min_bytes, int64_t *state_bytes);
+/* 1 if a non-finite R or C value was produced since create (blocks). */
+rikfad_status adafm_nonfinite(adafm_ctx *ctx, void *stream, int32_t *out);
+/* Per-step HIP event timing: ms4 = statistics pass, factor finalisation,
+ * RMS pass + scale, update pass (sums over the steps since enable/read). */
+rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable);
+rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms4, int64_t *steps);
+void adafm_destroy(adafm_ctx *ctx);
 
 /* ------------------------------------------------------------------------
  * Bandwidth probes (measurement aids for the HBM roofline).

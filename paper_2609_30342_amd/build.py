@@ -30,7 +30,7 @@ def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     hipcc = os.path.join(ROCM, "bin", "hipcc")
     objs = []
-    for src in ("kernels.hip", "diag.hip"):
+    for src in ("kernels.hip", "adafactor.hip", "diag.hip"):
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)

@@ -6,12 +6,14 @@
 // except the calls documented as blocking.
 #include <hip/hip_runtime_api.h>
 
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <string>
 #include <vector>
 
 #include "../../include/rikfad.h"
+#include "adafactor.hpp"
 #include "kernels.hpp"
 #include "plan.hpp"
 
@@ -127,15 +129,18 @@ struct GradRing {
     }
 };
 
-// Per-step event timing (benchmarks only).
+// Per-step event timing (benchmarks only): `per` events per step, one
+// before the first launch and one after each timed phase.
 struct Timing {
+    explicit Timing(int per_step = 4) : per(per_step) {}
+    int per;
     bool on = false;
-    std::vector<hipEvent_t> ev;     // 4 per step: before, after stream, after finalize, after apply
+    std::vector<hipEvent_t> ev;
     int64_t steps = 0;
 
     rikfad_status mark(int64_t step, int slot, hipStream_t stream)
     {
-        const size_t idx = static_cast<size_t>(step * 4 + slot);
+        const size_t idx = static_cast<size_t>(step * per + slot);
         while (ev.size() <= idx) {
             hipEvent_t e;
             HIP_TRY(hipEventCreate(&e), "hipEventCreate timing");
@@ -164,6 +169,21 @@ struct rikfad_ctx {
     bool pending = false;       // a deferred C.4 + D is owed to the matrices' p
     bool sums_valid = false;    // partial sums of R reflect the current R
     std::vector<const void *> grads_host;
+};
+
+struct adafm_ctx {
+    rk::Plan plan;
+    DeviceTables dev;
+    GradRing ring;
+    Timing timing{5};
+    adafm_hparams hp{};
+    int64_t steps = 0;                      // steps taken
+    std::vector<rk::TensorRange> ranges;    // tiles of each tensor
+    rk::TensorRange *ranges_dev = nullptr;
+    float *tilepart = nullptr;              // 2 per tile: sums of U^2 and X^2
+    float *scales = nullptr;                // 1 per tensor
+    std::vector<const void *> grads_host;
+    int64_t min_bytes = 0, update_bytes = 0;
 };
 
 struct ikfad_ctx {
@@ -377,19 +397,21 @@ rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out)
     return RIKFAD_OK;
 }
 
-static rikfad_status read_timing(Timing &tm, double *ms3, int64_t *steps)
+// Sums over the timed steps of the per - 1 phase durations into ms[].
+static rikfad_status read_timing(Timing &tm, double *ms, int64_t *steps)
 {
-    ms3[0] = ms3[1] = ms3[2] = 0.0;
+    const int per = tm.per;
+    for (int k = 0; k + 1 < per; ++k) ms[k] = 0.0;
     if (tm.steps > 0) {
-        HIP_TRY(hipEventSynchronize(tm.ev[static_cast<size_t>(tm.steps * 4 - 1)]),
+        HIP_TRY(hipEventSynchronize(tm.ev[static_cast<size_t>(tm.steps * per - 1)]),
                 "hipEventSynchronize timing");
         for (int64_t s = 0; s < tm.steps; ++s) {
-            for (int k = 0; k < 3; ++k) {
-                float ms = 0.f;
-                HIP_TRY(hipEventElapsedTime(&ms, tm.ev[static_cast<size_t>(s * 4 + k)],
-                                            tm.ev[static_cast<size_t>(s * 4 + k + 1)]),
+            for (int k = 0; k + 1 < per; ++k) {
+                float t = 0.f;
+                HIP_TRY(hipEventElapsedTime(&t, tm.ev[static_cast<size_t>(s * per + k)],
+                                            tm.ev[static_cast<size_t>(s * per + k + 1)]),
                         "hipEventElapsedTime");
-                ms3[k] += ms;
+                ms[k] += t;
             }
         }
     }
@@ -511,6 +533,278 @@ void ikfad_destroy(ikfad_ctx *ctx)
     if (!ctx) return;
     free_tables(ctx->dev);
     ctx->timing.release();
+    delete ctx;
+}
+
+// ------------------------------------------------------------ Adafactor-m
+
+static rikfad_status check_adafm_hparams(const adafm_hparams *hp)
+{
+    if (!hp) return fail(RIKFAD_EINVAL, "hparams is NULL");
+    if (hp->reserved != 0) return fail(RIKFAD_EINVAL, "reserved field must be 0");
+    if (!(std::isfinite(hp->h) && std::isfinite(hp->beta1) && std::isfinite(hp->decay_rate) &&
+          std::isfinite(hp->eps1) && std::isfinite(hp->eps2) &&
+          std::isfinite(hp->clip_threshold)))
+        return fail(RIKFAD_EINVAL, "hyperparameters must be finite");
+    if (!(hp->h > 0) || !(hp->beta1 >= 0 && hp->beta1 < 1) || !(hp->decay_rate <= 0) ||
+        !(hp->eps1 >= 0) || !(hp->eps2 >= 0) ||
+        (hp->scale_parameter != 0 && hp->scale_parameter != 1))
+        return fail(RIKFAD_EINVAL,
+                    "need h > 0, 0 <= beta1 < 1, decay_rate <= 0, eps1 >= 0, eps2 >= 0, "
+                    "scale_parameter 0 or 1");
+    const float fh = static_cast<float>(hp->h), fc = static_cast<float>(hp->clip_threshold);
+    const float fe1 = static_cast<float>(hp->eps1), fe2 = static_cast<float>(hp->eps2);
+    if (!(std::isfinite(fh) && fh > 0 && std::isfinite(fc) && std::isfinite(fe1) &&
+          std::isfinite(fe2)))
+        return fail(RIKFAD_EINVAL, "hyperparameters outside the fp32 range");
+    return RIKFAD_OK;
+}
+
+// Coefficients of step t (>= 1): b = 1 - t^decay_rate with 1 - b taken as
+// t^decay_rate itself, in fp64, each rounded once to fp32.
+static rk::AdaCoeffs adafm_coeffs(const adafm_hparams &hp, int64_t t)
+{
+    const double p = std::pow(static_cast<double>(t), hp.decay_rate);
+    rk::AdaCoeffs k{};
+    k.b = static_cast<float>(1.0 - p);
+    k.omb = static_cast<float>(p);
+    k.eps1 = static_cast<float>(hp.eps1);
+    k.beta1 = static_cast<float>(hp.beta1);
+    k.omb1 = static_cast<float>(1.0 - hp.beta1);
+    k.h = static_cast<float>(hp.h);
+    k.eps2 = static_cast<float>(hp.eps2);
+    k.clip = static_cast<float>(hp.clip_threshold);
+    k.scale = hp.scale_parameter;
+    return k;
+}
+
+static void adafm_free(adafm_ctx *ctx)
+{
+    free_tables(ctx->dev);
+    ctx->ring.release();
+    ctx->timing.release();
+    if (ctx->ranges_dev) (void)hipFree(ctx->ranges_dev);
+    if (ctx->tilepart) (void)hipFree(ctx->tilepart);
+    if (ctx->scales) (void)hipFree(ctx->scales);
+    ctx->ranges_dev = nullptr;
+    ctx->tilepart = nullptr;
+    ctx->scales = nullptr;
+}
+
+// Tile range of every tensor (the planner emits each tensor's tiles
+// contiguously) and the byte counts of the step.
+static rikfad_status adafm_layout(adafm_ctx *ctx)
+{
+    const rk::Plan &pl = ctx->plan;
+    const size_t nt = pl.tensors.size();
+    ctx->ranges.assign(nt, rk::TensorRange{-1, 0, 0});
+    for (size_t q = 0; q < pl.tiles.size(); ++q) {
+        rk::TensorRange &r = ctx->ranges[static_cast<size_t>(pl.tiles[q].tensor)];
+        if (r.tile0 < 0) r.tile0 = static_cast<int64_t>(q);
+        if (r.tile0 + r.ntile != static_cast<int64_t>(q))
+            return fail(RIKFAD_EINVAL, "internal: tiles of a tensor are not contiguous");
+        r.ntile += 1;
+    }
+    const int64_t sc = ctx->hp.scale_parameter ? 1 : 0, cl = ctx->hp.clip_threshold > 0 ? 1 : 0;
+    ctx->min_bytes = ctx->update_bytes = 0;
+    for (size_t i = 0; i < nt; ++i) {
+        const rk::TensorDesc &d = pl.tensors[i];
+        const int64_t mn = d.m * d.n, eb = d.dtype == rk::DT_BF16 ? 2 : 4;
+        ctx->ranges[i].elems = mn;
+        if (ctx->ranges[i].tile0 < 0) ctx->ranges[i].tile0 = 0;
+        if (d.kind == rk::KIND_VECTOR) {
+            // pass 1: g, v in, v out (+x); pass 3: g, x, M, v in, x, M out
+            ctx->min_bytes += mn * ((1 + sc) * eb + 8 + 3 * eb + 12);
+            ctx->update_bytes += mn * (3 * eb + 12);
+        } else {
+            // pass 1: g (+x); pass 2: g (with clipping); pass 3: g, x, M in, x, M out; R, C
+            ctx->min_bytes += mn * ((1 + sc + cl) * eb + 3 * eb + 8) + 8 * (d.m + d.n);
+            ctx->update_bytes += mn * (3 * eb + 8) + 4 * (d.m + d.n);
+        }
+    }
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_create(const rikfad_tensor *tensors, int64_t count, const adafm_hparams *hp,
+                           adafm_ctx **out)
+{
+    if (!out) return fail(RIKFAD_EINVAL, "out is NULL");
+    *out = nullptr;
+    rikfad_status s = check_adafm_hparams(hp);
+    if (s != RIKFAD_OK) return s;
+    adafm_ctx *ctx = new (std::nothrow) adafm_ctx();
+    if (!ctx) return fail(RIKFAD_ENOMEM, "host allocation failed");
+    std::string err;
+    if ((s = rk::plan_rikfad(tensors, count, ctx->plan, err)) != RIKFAD_OK) {
+        delete ctx;
+        return fail(s, err);
+    }
+    ctx->hp = *hp;
+    ctx->grads_host = ctx->plan.grads;
+    const size_t ntile = ctx->plan.tiles.size(), nt = ctx->plan.tensors.size();
+    if ((s = adafm_layout(ctx)) != RIKFAD_OK ||
+        (s = make_tables(ctx->plan, ctx->dev)) != RIKFAD_OK ||
+        (s = ctx->ring.init(nt)) != RIKFAD_OK ||
+        (s = upload(&ctx->ranges_dev, ctx->ranges, "hipMalloc/copy tensor ranges")) != RIKFAD_OK) {
+        std::string keep = g_last_error;
+        adafm_free(ctx);
+        delete ctx;
+        g_last_error = keep;
+        return s;
+    }
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&ctx->tilepart),
+                             sizeof(float) * 2 * (ntile ? ntile : 1));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&ctx->scales), sizeof(float) * (nt ? nt : 1));
+    if (e != hipSuccess) {
+        adafm_free(ctx);
+        delete ctx;
+        return hip_fail(e, "hipMalloc Adafactor-m workspace");
+    }
+    *out = ctx;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_step(adafm_ctx *ctx, void *stream_)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    hipStream_t stream = static_cast<hipStream_t>(stream_);
+    const rk::Plan &pl = ctx->plan;
+    const int64_t t = ctx->steps + 1;
+    if (pl.tiles.empty()) {
+        ctx->steps = t;
+        return RIKFAD_OK;
+    }
+    const rk::AdaCoeffs k = adafm_coeffs(ctx->hp, t);
+    rk::Coeffs fk{};            // the factor update R <- b R + (1-b) rowsum
+    fk.a = k.b;
+    fk.kappa = k.omb;
+    const int ng = static_cast<int>(pl.groups.size());
+    Timing &tm = ctx->timing;
+    rikfad_status s;
+    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    hipError_t e = rk::launch_adafm_stats(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
+                                          pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, k,
+                                          ctx->hp.scale_parameter != 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch adafm stats kernel");
+    if (tm.on && (s = tm.mark(tm.steps, 1, stream)) != RIKFAD_OK) return s;
+    const int64_t nfin = static_cast<int64_t>(pl.fin.size());
+    if (nfin > 0) {
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin - pl.fold_items, ctx->dev.ws,
+                                fk, ctx->dev.flag, 0, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
+        if (pl.fold_items > 0) {
+            e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + (nfin - pl.fold_items),
+                                    pl.fold_items, ctx->dev.ws, fk, ctx->dev.flag, 0, stream);
+            if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
+        }
+    }
+    if (tm.on && (s = tm.mark(tm.steps, 2, stream)) != RIKFAD_OK) return s;
+    if (ctx->hp.clip_threshold > 0 && pl.matrix_tiles > 0) {
+        e = rk::launch_adafm_rms(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
+                                 pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, stream);
+        if (e != hipSuccess) return hip_fail(e, "launch adafm rms kernel");
+    }
+    e = rk::launch_adafm_scale(ctx->ranges_dev, static_cast<int64_t>(pl.tensors.size()),
+                               ctx->tilepart, ctx->scales, k, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch adafm scale kernel");
+    if (tm.on && (s = tm.mark(tm.steps, 3, stream)) != RIKFAD_OK) return s;
+    e = rk::launch_adafm_update(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles, pl.groups.data(),
+                                ng, ctx->dev.ws, ctx->scales, k, stream);
+    if (e != hipSuccess) return hip_fail(e, "launch adafm update kernel");
+    if (tm.on) {
+        if ((s = tm.mark(tm.steps, 4, stream)) != RIKFAD_OK) return s;
+        tm.steps += 1;
+    }
+    ctx->steps = t;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_step_grads(adafm_ctx *ctx, const void *const *grads, void *stream)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    const size_t n = ctx->plan.tensors.size();
+    if (n > 0 && !grads) return fail(RIKFAD_EINVAL, "grads is NULL");
+    bool changed = false;
+    for (size_t i = 0; i < n; ++i) {
+        const rk::TensorDesc &d = ctx->plan.tensors[i];
+        if (!rk::grad_fits(grads[i], d.dtype, d.vec))
+            return fail(grads[i] ? RIKFAD_EALIGN : RIKFAD_EINVAL,
+                        "gradient " + std::to_string(i) +
+                            " is NULL or breaks the alignment planned at create");
+        changed = changed || grads[i] != ctx->grads_host[i];
+    }
+    if (changed) {
+        rikfad_status s = ctx->ring.push(ctx->dev.grads, grads, static_cast<hipStream_t>(stream));
+        if (s != RIKFAD_OK) return s;
+        for (size_t i = 0; i < n; ++i) ctx->grads_host[i] = grads[i];
+    }
+    return adafm_step(ctx, stream);
+}
+
+rikfad_status adafm_set_hparams(adafm_ctx *ctx, const adafm_hparams *hp)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    rikfad_status s = check_adafm_hparams(hp);
+    if (s != RIKFAD_OK) return s;
+    ctx->hp = *hp;
+    return adafm_layout(ctx);
+}
+
+rikfad_status adafm_set_step(adafm_ctx *ctx, int64_t steps_taken)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    if (steps_taken < 0) return fail(RIKFAD_EINVAL, "steps_taken must be >= 0");
+    ctx->steps = steps_taken;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_get_step(const adafm_ctx *ctx, int64_t *steps_taken)
+{
+    if (!ctx || !steps_taken) return fail(RIKFAD_EINVAL, "ctx or out is NULL");
+    *steps_taken = ctx->steps;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_min_bytes(const adafm_ctx *ctx, int64_t *min_bytes_per_step,
+                              int64_t *update_min_bytes, int64_t *state_bytes)
+{
+    if (!ctx || !min_bytes_per_step || !update_min_bytes || !state_bytes)
+        return fail(RIKFAD_EINVAL, "NULL argument");
+    *min_bytes_per_step = ctx->min_bytes;
+    *update_min_bytes = ctx->update_bytes;
+    *state_bytes = ctx->plan.state_bytes;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_nonfinite(adafm_ctx *ctx, void *stream, int32_t *out)
+{
+    if (!ctx || !out) return fail(RIKFAD_EINVAL, "ctx or out is NULL");
+    HIP_TRY(hipStreamSynchronize(static_cast<hipStream_t>(stream)), "hipStreamSynchronize");
+    int v = 0;
+    HIP_TRY(hipMemcpy(&v, ctx->dev.flag, sizeof(int), hipMemcpyDeviceToHost), "hipMemcpy flag");
+    *out = v ? 1 : 0;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable)
+{
+    if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
+    ctx->timing.on = enable != 0;
+    ctx->timing.steps = 0;
+    return RIKFAD_OK;
+}
+
+rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms4, int64_t *steps)
+{
+    if (!ctx || !ms4 || !steps) return fail(RIKFAD_EINVAL, "NULL argument");
+    return read_timing(ctx->timing, ms4, steps);
+}
+
+void adafm_destroy(adafm_ctx *ctx)
+{
+    if (!ctx) return;
+    adafm_free(ctx);
     delete ctx;
 }
 

@@ -110,4 +110,25 @@ struct Coeffs {
     float eps;         // eps_stab
 };
 
+// Adafactor-m step coefficients (fp64 on the host, rounded once).
+struct AdaCoeffs {
+    float b;           // beta2_t = 1 - t^decay_rate
+    float omb;         // 1 - beta2_t
+    float eps1;        // added to G^2
+    float beta1;       // first-moment decay
+    float omb1;        // 1 - beta1
+    float h;           // step size
+    float eps2;        // floor of RMS(X) in the parameter scale
+    float clip;        // update clipping threshold (<= 0: off)
+    int32_t scale;     // parameter scaling on
+    int32_t pad;
+};
+
+// Tiles of one tensor in the tile table (they are contiguous).
+struct TensorRange {
+    int64_t tile0;
+    int64_t ntile;
+    int64_t elems;
+};
+
 }  // namespace rk

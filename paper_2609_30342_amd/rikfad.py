@@ -1,8 +1,8 @@
 """ctypes binding of librikfad.so (declared in include/rikfad.h).
 
 Argument marshalling only: every step of the optimiser runs in the library's
-HIP kernels.  The functions keep the C names; ``RIKFAD`` and ``IKFAD`` are
-small conveniences that collect device pointers from torch tensors and
+HIP kernels.  The functions keep the C names; ``RIKFAD``, ``IKFAD`` and
+``ADAFM`` (the Adafactor-m baseline) are small conveniences that collect device pointers from torch tensors and
 allocate the optimiser state as zero-filled torch tensors.  There is no CPU
 fallback: if the library is missing, every call raises.
 """
@@ -53,6 +53,13 @@ class rikfad_info(ctypes.Structure):
         "finalize_items")] + [("pending", ctypes.c_int32), ("two_pass", ctypes.c_int32)]
 
 
+class adafm_hparams(ctypes.Structure):
+    _fields_ = [("h", ctypes.c_double), ("beta1", ctypes.c_double),
+                ("decay_rate", ctypes.c_double), ("eps1", ctypes.c_double),
+                ("eps2", ctypes.c_double), ("clip_threshold", ctypes.c_double),
+                ("scale_parameter", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class rikfad_friction_stats(ctypes.Structure):
     _fields_ = [(nm, ctypes.c_double) for nm in (
         "xi_fro2", "err_fro2", "sum_r", "sigma1", "rel_err", "eckart_young_floor",
@@ -89,6 +96,17 @@ _SIGNATURES = {
     "ikfad_destroy": (None, [_vp]),
     "rikfad_friction_report": (_st, [_vp, _i64, _i64, ctypes.c_double, _i32, _vp,
                                      _P(rikfad_friction_stats)]),
+    "adafm_create": (_st, [_vp, _i64, _P(adafm_hparams), _P(_vp)]),
+    "adafm_step": (_st, [_vp, _vp]),
+    "adafm_step_grads": (_st, [_vp, _vp, _vp]),
+    "adafm_set_hparams": (_st, [_vp, _P(adafm_hparams)]),
+    "adafm_set_step": (_st, [_vp, _i64]),
+    "adafm_get_step": (_st, [_vp, _P(_i64)]),
+    "adafm_min_bytes": (_st, [_vp, _P(_i64), _P(_i64), _P(_i64)]),
+    "adafm_nonfinite": (_st, [_vp, _vp, _P(_i32)]),
+    "adafm_timing_enable": (_st, [_vp, _i32]),
+    "adafm_timing_read": (_st, [_vp, _P(ctypes.c_double), _P(_i64)]),
+    "adafm_destroy": (None, [_vp]),
     "rikfad_probe_stream": (_st, [_vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "rikfad_probe_copy": (_st, [_vp, _vp, _i64, _vp]),
 }
@@ -248,6 +266,75 @@ def rikfad_probe_copy(src, dst, nbytes, stream=None):
     _check(lib().rikfad_probe_copy(src, dst, int(nbytes), stream), "rikfad_probe_copy")
 
 
+def adafm_params(h, beta1=0.9, decay_rate=-0.8, eps1=1e-30, eps2=1e-3, clip_threshold=1.0,
+                 scale_parameter=False):
+    return adafm_hparams(float(h), float(beta1), float(decay_rate), float(eps1), float(eps2),
+                         float(clip_threshold), int(bool(scale_parameter)), 0)
+
+
+def adafm_create(tensors, hp):
+    arr = _array(tensors, rikfad_tensor)
+    ctx = ctypes.c_void_p()
+    _check(lib().adafm_create(ctypes.addressof(arr), len(tensors), ctypes.byref(hp),
+                              ctypes.byref(ctx)), "adafm_create")
+    return ctx
+
+
+def adafm_step(ctx, stream=None):
+    _check(lib().adafm_step(ctx, stream), "adafm_step")
+
+
+def adafm_step_grads(ctx, grads, stream=None):
+    arr = (ctypes.c_void_p * max(1, len(grads)))(*grads)
+    _check(lib().adafm_step_grads(ctx, ctypes.addressof(arr), stream), "adafm_step_grads")
+
+
+def adafm_set_hparams(ctx, hp):
+    _check(lib().adafm_set_hparams(ctx, ctypes.byref(hp)), "adafm_set_hparams")
+
+
+def adafm_set_step(ctx, steps_taken):
+    _check(lib().adafm_set_step(ctx, int(steps_taken)), "adafm_set_step")
+
+
+def adafm_get_step(ctx):
+    v = ctypes.c_int64()
+    _check(lib().adafm_get_step(ctx, ctypes.byref(v)), "adafm_get_step")
+    return v.value
+
+
+def adafm_min_bytes(ctx):
+    """(bytes per step, bytes of the update pass, state bytes)."""
+    a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().adafm_min_bytes(ctx, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)),
+           "adafm_min_bytes")
+    return a.value, b.value, c.value
+
+
+def adafm_nonfinite(ctx, stream=None):
+    v = ctypes.c_int32()
+    _check(lib().adafm_nonfinite(ctx, stream, ctypes.byref(v)), "adafm_nonfinite")
+    return bool(v.value)
+
+
+def adafm_timing_enable(ctx, enable=True):
+    _check(lib().adafm_timing_enable(ctx, int(bool(enable))), "adafm_timing_enable")
+
+
+def adafm_timing_read(ctx):
+    """(ms of the statistics pass, finalisation, RMS pass + scale, update
+    pass) summed over the timed steps, and the step count."""
+    ms = (ctypes.c_double * 4)()
+    steps = ctypes.c_int64()
+    _check(lib().adafm_timing_read(ctx, ms, ctypes.byref(steps)), "adafm_timing_read")
+    return tuple(ms), steps.value
+
+
+def adafm_destroy(ctx):
+    if ctx:
+        lib().adafm_destroy(ctx)
+
+
 # ------------------------------------------------------------- torch glue
 
 def _dtype_code(t):
@@ -369,6 +456,62 @@ class IKFAD:
 
     def close(self):
         ikfad_destroy(self.ctx)
+        self.ctx = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "ctx", None):
+                self.close()
+        except Exception:
+            pass
+
+
+class ADAFM:
+    """Adafactor-m (the paper's baseline) over (parameter, gradient) pairs.
+
+    Same tensor conventions as ``RIKFAD``: state is the first moment
+    (m x n fp32) and the second-moment factors r (m), c (n); a vector keeps
+    its unfactored second moment in c (1 x n) or r (m x 1).
+    """
+
+    def __init__(self, params, grads, h, beta1=0.9, decay_rate=-0.8, eps1=1e-30, eps2=1e-3,
+                 clip_threshold=1.0, scale_parameter=False, state=None):
+        import torch
+        self.params, self.grads, self.state = list(params), list(grads), []
+        structs = []
+        for i, (x, g) in enumerate(zip(self.params, self.grads)):
+            if not (x.is_cuda and g.is_cuda and x.is_contiguous() and g.is_contiguous()):
+                raise ValueError(f"tensor {i}: parameters and gradients must be contiguous "
+                                 "device tensors")
+            if g.dtype != x.dtype or g.numel() != x.numel():
+                raise ValueError(f"tensor {i}: gradient does not match its parameter")
+            m, n = _shape2(x)
+            if state is not None:
+                mom, r, c = state[i]
+            else:
+                mom = torch.zeros((m, n), device=x.device, dtype=torch.float32)
+                r = torch.zeros(m, device=x.device, dtype=torch.float32)
+                c = torch.zeros(n, device=x.device, dtype=torch.float32)
+            self.state.append((mom, r, c))
+            structs.append(rikfad_tensor(x.data_ptr(), g.data_ptr(), mom.data_ptr(),
+                                         r.data_ptr(), c.data_ptr(), m, n, _dtype_code(x), 0))
+        self.hp = adafm_params(h, beta1, decay_rate, eps1, eps2, clip_threshold, scale_parameter)
+        self.ctx = adafm_create(structs, self.hp)
+
+    def step(self, grads=None, stream=None):
+        s = _stream_handle(stream)
+        if grads is None:
+            adafm_step(self.ctx, s)
+        else:
+            self.grads = list(grads)
+            adafm_step_grads(self.ctx, [g.data_ptr() for g in self.grads], s)
+
+    @property
+    def steps_taken(self):
+        return adafm_get_step(self.ctx)
+
+    def close(self):
+        adafm_destroy(self.ctx)
         self.ctx = None
 
     def __del__(self):

@@ -87,12 +87,10 @@ class Pair:
     checked: list        # indices the oracle follows
 
 
-def make_pair(specs, hp, seed=0, scales="lognormal", two_pass=False, checked=None,
-              device="cuda:0", x_offset=0):
-    """x_offset > 0 places each parameter and gradient that many elements into
+def _buffers(specs, wl, checked, seed, device, x_offset):
+    """Device parameters (the workload's initial values) and gradient buffers.
+    x_offset > 0 places each parameter and gradient that many elements into
     a larger buffer (misaligned views, scalar path)."""
-    wl = synth.Workload(specs, seed=seed, scales=scales)
-    checked = list(range(len(specs))) if checked is None else list(checked)
     xs, gs = [], []
     for i, sp in enumerate(specs):
         dt = torch.bfloat16 if sp.dtype == "bf16" else torch.float32
@@ -112,11 +110,22 @@ def make_pair(specs, hp, seed=0, scales="lognormal", two_pass=False, checked=Non
             g = torch.empty_like(x)
         xs.append(x)
         gs.append(g)
+    return xs, gs
+
+
+def _oracle_state(specs, wl, checked):
+    return {i: O.make_tensor(wl.x0(i).astype(np.float64), bf16=(specs[i].dtype == "bf16"),
+                             track_unrounded=(specs[i].dtype == "bf16"))
+            for i in checked}
+
+
+def make_pair(specs, hp, seed=0, scales="lognormal", two_pass=False, checked=None,
+              device="cuda:0", x_offset=0):
+    wl = synth.Workload(specs, seed=seed, scales=scales)
+    checked = list(range(len(specs))) if checked is None else list(checked)
+    xs, gs = _buffers(specs, wl, checked, seed, device, x_offset)
     opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
-    ref = {i: O.make_tensor(wl.x0(i).astype(np.float64), bf16=(specs[i].dtype == "bf16"),
-                            track_unrounded=(specs[i].dtype == "bf16"))
-           for i in checked}
-    return Pair(specs, wl, xs, gs, opt, ref, checked)
+    return Pair(specs, wl, xs, gs, opt, _oracle_state(specs, wl, checked), checked)
 
 
 def load_grads(pair, step, seed_unchecked=0):
@@ -220,3 +229,84 @@ def run_parity(specs, hp, steps, seed=0, scales="lognormal", two_pass=False, che
         errs["x_bf16"] = max(errs["x_bf16"], worst["x_bf16"])
     log(f"[parity] {label} steps={steps} errs={ {k: f'{v:.2e}' for k, v in errs.items()} }")
     return pair, errs
+
+
+# ------------------------------------------------------------- Adafactor-m
+
+@dataclass
+class AdafmPair:
+    specs: list
+    wl: synth.Workload
+    xs: list
+    gs: list
+    opt: R.ADAFM
+    ref: dict
+    checked: list
+
+
+def make_adafm_pair(specs, hp, seed=0, scales="lognormal", checked=None, device="cuda:0",
+                    x_offset=0):
+    """Adafactor-m context over the workload's initial parameters, with the
+    oracle following the `checked` tensors (all by default)."""
+    wl = synth.Workload(specs, seed=seed, scales=scales)
+    checked = list(range(len(specs))) if checked is None else list(checked)
+    xs, gs = _buffers(specs, wl, checked, seed, device, x_offset)
+    opt = R.ADAFM(xs, gs, **hp)
+    return AdafmPair(specs, wl, xs, gs, opt, _oracle_state(specs, wl, checked), checked)
+
+
+def adafm_oracle_step(pair, host_g, t, hp, threads=16):
+    idx = sorted(pair.ref)
+    O.adafm_step_list([pair.ref[i] for i in idx], [host_g[i] for i in idx], t,
+                      O.AdafmHParams(**hp), threads=threads)
+
+
+def compare_adafm(pair):
+    """Errors of x, the first moment M (``p``), the factors R, C and the
+    unfactored second moment of vectors (``r``), as in ``compare``."""
+    torch.cuda.synchronize()
+    errs = {"x": 0.0, "x_elem": 0.0, "x_bf16": 0.0, "p": 0.0, "p_elem": 0.0, "r": 0.0,
+            "c": 0.0}
+    for i, o in pair.ref.items():
+        mom, r, c = pair.opt.state[i]
+        if o.bf16:
+            errs["x_bf16"] = max(errs["x_bf16"], rel_rms(host(pair.xs[i]), o.x_unrounded))
+        else:
+            xg = host(pair.xs[i])
+            errs["x"] = max(errs["x"], rel_norm(xg, o.x))
+            errs["x_elem"] = max(errs["x_elem"], rel_rms(xg, o.x))
+        mg = host(mom)
+        errs["p"] = max(errs["p"], rel_norm(mg, o.p))
+        errs["p_elem"] = max(errs["p_elem"], rel_rms(mg, o.p))
+        if o.is_vector:
+            errs["r"] = max(errs["r"], rel_plain(host(c if o.m == 1 else r), o.xi))
+        else:
+            errs["r"] = max(errs["r"], rel_plain(host(r), o.r))
+            errs["c"] = max(errs["c"], rel_plain(host(c), o.c))
+    return errs
+
+
+def run_adafm_parity(specs, hp, steps, seed=0, scales="lognormal", checked=None, label="",
+                     x_offset=0, first_step=1, threads=16):
+    """`steps` Adafactor-m steps t = first_step, first_step + 1, ... on the GPU
+    and in the oracle from the same inputs; bf16 parameters are reset to the
+    oracle's before every step and compared with its unrounded update."""
+    pair = make_adafm_pair(specs, hp, seed=seed, scales=scales, checked=checked,
+                           x_offset=x_offset)
+    if first_step > 1:
+        R.adafm_set_step(pair.opt.ctx, first_step - 1)
+    has_bf16 = any(pair.ref[i].bf16 for i in pair.ref)
+    worst = {}
+    for s in range(steps):
+        t = first_step + s
+        log(f"[adafm] {label} step t={t}")
+        if has_bf16:
+            reset_bf16_x(pair)
+        hg = load_grads(pair, s, seed)
+        pair.opt.step()
+        adafm_oracle_step(pair, hg, t, hp, threads=threads)
+        e = compare_adafm(pair)
+        for k, v in e.items():
+            worst[k] = max(worst.get(k, 0.0), v)
+    log(f"[adafm] {label} steps={steps} errs={ {k: f'{v:.2e}' for k, v in worst.items()} }")
+    return pair, worst

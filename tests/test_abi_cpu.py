@@ -178,3 +178,62 @@ def test_state_is_order_m_plus_n_per_matrix():
         rk, ik = R.rikfad_state_bytes([_t(m=m, n=n)])
         assert rk - 4 * m * n == 4 * (m + n)
         assert ik - 4 * m * n == 4 * m * n
+
+
+def _adafm_status(tensors, hp=None):
+    hp = hp or R.adafm_params(1e-3)
+    arr = R._array(tensors, R.rikfad_tensor)
+    ctx = ctypes.c_void_p()
+    st = R.lib().adafm_create(ctypes.addressof(arr), len(tensors), ctypes.byref(hp),
+                              ctypes.byref(ctx))
+    if st != R.RIKFAD_OK:
+        assert not ctx.value
+    else:
+        R.adafm_destroy(ctx)
+    return st
+
+
+@pytest.mark.parametrize("hp", [
+    dict(h=0.0), dict(h=-1.0), dict(h=1e-3, beta1=1.0), dict(h=1e-3, beta1=-0.1),
+    dict(h=1e-3, decay_rate=0.5), dict(h=1e-3, eps1=-1e-30), dict(h=1e-3, eps2=-1.0),
+    dict(h=1e-3, clip_threshold=float("nan")), dict(h=float("inf")), dict(h=1e39),
+])
+def test_adafm_create_rejects_bad_hparams(hp):
+    assert _adafm_status([_t()], hp=R.adafm_params(**hp)) == R.RIKFAD_EINVAL
+    assert R.rikfad_last_error()
+
+
+def test_adafm_create_rejects_bad_flags_tensors_and_nulls():
+    hp = R.adafm_params(1e-3)
+    hp.scale_parameter = 2
+    assert _adafm_status([_t()], hp=hp) == R.RIKFAD_EINVAL
+    hp = R.adafm_params(1e-3)
+    hp.reserved = 1
+    assert _adafm_status([_t()], hp=hp) == R.RIKFAD_EINVAL
+    assert _adafm_status([_t(m=0)]) == R.RIKFAD_EINVAL
+    assert _adafm_status([_t(x=BASE + 2)]) == R.RIKFAD_EALIGN
+    assert _adafm_status([_t(m=1, n=16, c=None)]) == R.RIKFAD_EINVAL   # v lives in c
+    L = R.lib()
+    ctx = ctypes.c_void_p()
+    arr = R._array([_t()], R.rikfad_tensor)
+    assert L.adafm_create(ctypes.addressof(arr), 1, None, ctypes.byref(ctx)) == R.RIKFAD_EINVAL
+    assert L.adafm_create(ctypes.addressof(arr), 1, ctypes.byref(R.adafm_params(1e-3)),
+                          None) == R.RIKFAD_EINVAL
+    assert L.adafm_step(None, None) == R.RIKFAD_EINVAL
+    assert L.adafm_set_step(None, 3) == R.RIKFAD_EINVAL
+    L.adafm_destroy(None)
+
+
+def test_adafm_state_equals_rikfad_state():
+    """App. "Memory Analysis", Table "Optimizer auxiliary state": Adafactor-m
+    with its first moment carries the same auxiliary state as R-iKFAD (a
+    full m x n buffer plus O(m + n) factors; the full second moment of a
+    vector), which is why the paper compares the two at matched memory."""
+    gold = {}
+    for line in open(os.path.join(ROOT, "tests", "golden", "memory_table.txt")):
+        if line.startswith("#") or not line.strip():
+            continue
+        f = line.split()
+        gold[f[0]] = dict(adafm=float(f[3]), rikfad=float(f[6]))
+    for name in gold:
+        assert gold[name]["adafm"] == gold[name]["rikfad"], name
