@@ -19,8 +19,9 @@ S = synth.TensorSpec
 
 @pytest.mark.parametrize("two_pass", [False, True])
 def test_graph_replays_match_eager_bitwise(two_pass):
+    # f: 66 row stripes, two column segments (the second finalisation launch)
     specs = [S("a", 256, 512), S("b", 1, 512), S("c", 300, 27), S("d", 40, 640, "bf16"),
-             S("e", 640, 1, "bf16")]
+             S("e", 640, 1, "bf16"), S("f", 4200, 96)]
     hp = synth.HP_FRICTION
     log(f"[case] graph capture two_pass={two_pass}")
     eager = make_pair(specs, hp, seed=21, two_pass=two_pass, checked=[])

@@ -77,6 +77,23 @@ def test_edge_shapes(name, specs):
     assert_ok(errs, label=name)
 
 
+SCHEDULE_CASES = [
+    ("tall_segments", [S("a", 9000, 64), S("b", 4200, 96, "bf16")]),
+    ("mixed", [S("a", 96, 200), S("b", 1, 200), S("c", 40, 640, "bf16"), S("d", 640, 1, "bf16"),
+               S("e", 2100, 1000)]),
+]
+
+
+@pytest.mark.parametrize("name,specs", SCHEDULE_CASES, ids=[c[0] for c in SCHEDULE_CASES])
+def test_multi_segment_finalisation(name, specs):
+    """Tensors with many row stripes and several column segments (the
+    second, segment-folding finalisation launch) against the oracle, in the
+    friction-active setting, 12 steps."""
+    log(f"[case] multi-segment {name}")
+    _, errs = run_parity(specs, synth.HP_FRICTION, 12, seed=8, label=f"multi-segment {name}")
+    assert_ok(errs, label=name)
+
+
 def test_misaligned_views_take_scalar_path():
     """Parameters and gradients that start one element into their buffers
     (not 16-byte aligned) still match the oracle."""
@@ -240,7 +257,8 @@ def _run_steps(specs, hp, steps, two_pass=False, seed=5):
     return pair
 
 
-SPECS_MIX = [S("a", 300, 520), S("b", 1, 520), S("c", 77, 1000, "bf16"), S("d", 129, 27)]
+SPECS_MIX = [S("a", 300, 520), S("b", 1, 520), S("c", 77, 1000, "bf16"), S("d", 129, 27),
+             S("e", 4200, 96)]          # e: 66 row stripes, two column segments
 
 
 def test_deterministic_bitwise():
