@@ -13,7 +13,9 @@
 // order): row sums one wave per row, column sums in row stripes then
 // folded in stripe order, squared norms per workgroup then folded in order.
 // sigma_1 comes from power iteration on xi^T xi started at C / |C| (xi >= 0,
-// so the leading singular vectors are non-negative), normalised on the GPU.
+// so the leading singular vectors are non-negative), normalised on the GPU:
+// the column fold also writes per-workgroup squared-norm partials, from
+// which every wave of the next row pass derives the same scale.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -26,6 +28,9 @@ namespace {
 constexpr int kT = 256;            // threads per workgroup
 constexpr int kStatChunk = 4096;   // elements per workgroup of the vector statistics
 constexpr int kErrRows = 16;       // rows per workgroup of the error pass
+constexpr int kFoldCols = 32;      // columns per workgroup of the column fold
+constexpr int kFoldGroups = 8;     // stripe groups per column of the column fold
+static_assert(kFoldCols * kFoldGroups == 256, "fold workgroup shape");
 
 #define DG __attribute__((address_space(1)))
 template <typename T> __device__ __forceinline__ const DG T *gp(const T *q) { return (const DG T *)q; }
@@ -39,16 +44,30 @@ __device__ __forceinline__ double wave_sum(double v)
     return v;
 }
 
-// out[i] = sum_j xi[i, j] * (w ? w[j] * (*wscale) : 1): one wave per row,
-// lanes stride over the columns, fp64 accumulation.
+// Scale of a vector from its fold partials: 1 / sqrt(sum_q parts[2 q]) in
+// a fixed order (lanes stride over the partials, then the butterfly), 0 for
+// a zero vector; every wave that calls it gets the same bits.
+__device__ __forceinline__ double inv_norm(const double *__restrict__ parts, int64_t nparts)
+{
+    const int lane = threadIdx.x & 63;
+    double s = 0.0;
+    for (int64_t q = lane; q < nparts; q += 64) s += gp(parts)[2 * q];
+    s = wave_sum(s);
+    return s > 0.0 ? 1.0 / sqrt(s) : 0.0;
+}
+
+// out[i] = sum_j xi[i, j] * (w ? w[j] * scale : 1) with scale = inv_norm of
+// w's fold partials: one wave per row, lanes stride over the columns, fp64
+// accumulation.
 __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict__ xi, int64_t m,
                                                         int64_t n, const double *__restrict__ w,
-                                                        const double *__restrict__ wscale,
-                                                        double *__restrict__ out)
+                                                        const double *__restrict__ wparts,
+                                                        int64_t nwparts, double *__restrict__ out)
 {
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (kT / 64) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= m) return;
+    const double scale = w ? inv_norm(wparts, nwparts) : 1.0;
     const DG float *xr = gp(xi) + row * n;
     double s = 0.0;
     // Eight loads in flight per lane; additions in column order.
@@ -63,7 +82,7 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
         for (int u = 0; u < 8; ++u) s += v[u];
     }
     s = wave_sum(s);
-    if (lane == 0) gp(out)[row] = w ? s * gp(wscale)[0] : s;
+    if (lane == 0) gp(out)[row] = w ? s * scale : s;
 }
 
 // part[s, j] = sum over rows i of stripe s of xi[i, j] * (w ? w[i] : 1).
@@ -92,23 +111,47 @@ __global__ __launch_bounds__(kT) void col_partial_kernel(const float *__restrict
     gp(part)[s * n + j] = acc;
 }
 
-// out[j] = (sum_s part[s, j]) * (wscale ? *wscale : 1), stripes in order.
+// out[j] = sum_s part[s, j]: a workgroup takes kFoldCols columns, its
+// kFoldGroups thread groups sum consecutive ranges of stripes in stripe
+// order and are added in group order.  The workgroup also writes
+// parts[2 b] = sum of out[j]^2 and parts[2 b + 1] = sum of out[j] over its
+// columns (in column order), the partials inv_norm and the statistics use.
 __global__ __launch_bounds__(kT) void col_fold_kernel(const double *__restrict__ part, int64_t n,
-                                                      int64_t nstripes,
-                                                      const double *__restrict__ wscale,
-                                                      double *__restrict__ out)
+                                                      int64_t nstripes, double *__restrict__ out,
+                                                      double *__restrict__ parts)
 {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kT + threadIdx.x;
-    if (j >= n) return;
+    __shared__ double l[kT];
+    const int c = threadIdx.x % kFoldCols, g = threadIdx.x / kFoldCols;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kFoldCols + c;
+    const int64_t per = (nstripes + kFoldGroups - 1) / kFoldGroups;
+    const int64_t s0 = g * per < nstripes ? g * per : nstripes;
+    const int64_t s1 = s0 + per < nstripes ? s0 + per : nstripes;
     double acc = 0.0;
-    for (int64_t s0 = 0; s0 < nstripes; s0 += 16) {
-        double v[16];
+    if (j < n) {
+        for (int64_t b = s0; b < s1; b += 16) {
+            double v[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = s0 + u < nstripes ? gp(part)[(s0 + u) * n + j] : 0.0;
+            for (int u = 0; u < 16; ++u) v[u] = b + u < s1 ? gp(part)[(b + u) * n + j] : 0.0;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) acc += v[u];
+            for (int u = 0; u < 16; ++u) acc += v[u];
+        }
     }
-    gp(out)[j] = wscale ? acc * gp(wscale)[0] : acc;
+    l[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double q2 = 0.0, q1 = 0.0;
+        for (int cc = 0; cc < kFoldCols; ++cc) {
+            const int64_t jj = static_cast<int64_t>(blockIdx.x) * kFoldCols + cc;
+            if (jj >= n) break;
+            double v = l[cc];
+            for (int gg = 1; gg < kFoldGroups; ++gg) v += l[gg * kFoldCols + cc];
+            gp(out)[jj] = v;
+            q2 += v * v;
+            q1 += v;
+        }
+        gp(parts)[2 * blockIdx.x] = q2;
+        gp(parts)[2 * blockIdx.x + 1] = q1;
+    }
 }
 
 // Workgroup b: part[2 b] = sum of v[k]^2 and part[2 b + 1] = sum of v[k]
@@ -144,10 +187,9 @@ __global__ __launch_bounds__(kT) void vec_stats_kernel(const double *__restrict_
     }
 }
 
-// res = the chunk statistics folded in chunk order; scale = 1 / sqrt(res[0])
-// (0 for a zero vector) when scale is given.
+// res = the chunk statistics folded in chunk order.
 __global__ void stats_fold_kernel(const double *__restrict__ part, int64_t nchunks,
-                                  double *__restrict__ res, double *__restrict__ scale)
+                                  double *__restrict__ res)
 {
     if (threadIdx.x == 0 && blockIdx.x == 0) {
         double a = 0.0, b = 0.0;
@@ -157,7 +199,6 @@ __global__ void stats_fold_kernel(const double *__restrict__ part, int64_t nchun
         }
         gp(res)[0] = a;
         gp(res)[1] = b;
-        if (scale) gp(scale)[0] = a > 0.0 ? 1.0 / sqrt(a) : 0.0;
     }
 }
 
@@ -202,18 +243,33 @@ __global__ __launch_bounds__(kT) void err_partial_kernel(const float *__restrict
     }
 }
 
-// res[0] = sum of part[2 k], res[1] = sum of part[2 k + 1], in k order.
-__global__ void err_fold_kernel(const double *__restrict__ part, int64_t nblk,
-                                double *__restrict__ res)
+// res[0] = sum of part[2 k], res[1] = sum of part[2 k + 1]: thread t sums
+// k = t, t + 256, ... in order, then the threads are combined in a fixed
+// order (butterfly in each wave, waves in order).
+__global__ __launch_bounds__(kT) void err_fold_kernel(const double *__restrict__ part, int64_t nblk,
+                                                      double *__restrict__ res)
 {
-    if (threadIdx.x == 0 && blockIdx.x == 0) {
-        double a = 0.0, b = 0.0;
-        for (int64_t q = 0; q < nblk; ++q) {
-            a += gp(part)[2 * q];
-            b += gp(part)[2 * q + 1];
+    __shared__ double la[kT / 64], lb[kT / 64];
+    double a = 0.0, b = 0.0;
+    for (int64_t q = threadIdx.x; q < nblk; q += kT) {
+        a += gp(part)[2 * q];
+        b += gp(part)[2 * q + 1];
+    }
+    a = wave_sum(a);
+    b = wave_sum(b);
+    if ((threadIdx.x & 63) == 0) {
+        la[threadIdx.x >> 6] = a;
+        lb[threadIdx.x >> 6] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double x = la[0], y = lb[0];
+        for (int w = 1; w < kT / 64; ++w) {
+            x += la[w];
+            y += lb[w];
         }
-        gp(res)[0] = a;
-        gp(res)[1] = b;
+        gp(res)[0] = x;
+        gp(res)[1] = y;
     }
 }
 
@@ -245,53 +301,59 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     while ((m + stripe - 1) / stripe > 65535) stripe <<= 1;
     const int64_t nstripes = (m + stripe - 1) / stripe;
     const int64_t nerr = (m + kErrRows - 1) / kErrRows;
+    const int64_t nfold = (n + kFoldCols - 1) / kFoldCols;
     const int64_t mk = m > n ? m : n;
     const int64_t nstat = (mk + kStatChunk - 1) / kStatChunk;
-    // workspace (doubles): r m, c n, u m, v n, colpart nstripes*n, errpart 2*nerr,
-    // statpart 2*nstat, stats 2 (r), 2 (v), 2 (u), 2 (err), scale 1
-    const int64_t words = m + n + m + n + nstripes * n + 2 * nerr + 2 * nstat + 9;
+    // workspace (doubles): r m, c n, u m, v n, column partials nstripes*n,
+    // error partials 2*nerr, fold partials 2*nfold (C) and 2*nfold (v),
+    // statistics partials 2*nstat, results 2 (R), 2 (u), 2 (errors)
+    const int64_t words = m + n + m + n + nstripes * n + 2 * nerr + 4 * nfold + 2 * nstat + 6;
     DevBuf buf;
     if (hipMalloc(&buf.p, sizeof(double) * static_cast<size_t>(words)) != hipSuccess)
         return RIKFAD_ENOMEM;
     double *r = static_cast<double *>(buf.p), *c = r + m, *u = c + n, *v = u + m;
-    double *cpart = v + n, *epart = cpart + nstripes * n, *spart = epart + 2 * nerr;
-    double *stats_r = spart + 2 * nstat, *stats_v = stats_r + 2, *stats_u = stats_v + 2;
-    double *err = stats_u + 2, *scale_v = err + 2;
+    double *cpart = v + n, *epart = cpart + nstripes * n, *cfold = epart + 2 * nerr;
+    double *vfold = cfold + 2 * nfold, *spart = vfold + 2 * nfold;
+    double *stats_r = spart + 2 * nstat, *stats_u = stats_r + 2, *err = stats_u + 2;
     const dim3 rows_grid(static_cast<uint32_t>((m + kT / 64 - 1) / (kT / 64)));
     const dim3 cols_grid(static_cast<uint32_t>(ncb), static_cast<uint32_t>(nstripes));
-    const dim3 fold_grid(static_cast<uint32_t>((n + kT - 1) / kT));
-    auto stats = [&](const double *vec, int64_t k, double *res, double *scale) {
+    const dim3 fold_grid(static_cast<uint32_t>(nfold));
+    auto stats = [&](const double *vec, int64_t k, double *res) {
         const int64_t nc = (k + kStatChunk - 1) / kStatChunk;
         hipLaunchKernelGGL(vec_stats_kernel, dim3(static_cast<uint32_t>(nc)), dim3(kT), 0, st, vec,
                            k, spart);
-        hipLaunchKernelGGL(stats_fold_kernel, dim3(1), dim3(1), 0, st, spart, nc, res, scale);
+        hipLaunchKernelGGL(stats_fold_kernel, dim3(1), dim3(1), 0, st, spart, nc, res);
     };
 
-    // Shadow factors R = xi 1, C = xi^T 1 and their totals.
-    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, nullptr, nullptr, r);
+    // Shadow factors R = xi 1, C = xi^T 1 and the sum of R.
+    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, nullptr, nullptr,
+                       int64_t(0), r);
     hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, nullptr,
                        cpart);
-    hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, nullptr, c);
-    stats(r, m, stats_r, nullptr);
+    hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, c, cfold);
+    stats(r, m, stats_r);
     // |xi|_F^2 and |xi - xi~|_F^2
     hipLaunchKernelGGL(err_partial_kernel, dim3(static_cast<uint32_t>(nerr)), dim3(kT), 0, st, xi,
                        m, n, r, c, stats_r, eps_stab, epart);
-    hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(1), 0, st, epart, nerr, err);
-    // Power iteration on xi^T xi from v = C / |C|: u = xi v, v <- xi^T u / |xi^T u|.
-    stats(c, n, stats_v, scale_v);
-    const double *vin = c;
+    hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(kT), 0, st, epart, nerr, err);
+    // Power iteration on xi^T xi from v = C / |C|: u = xi v / |v|, v <- xi^T u;
+    // each row pass normalises its input from the fold partials of the last
+    // column pass.
+    const double *vin = c, *vin_fold = cfold;
     for (int it = 0; it < power_iters; ++it) {
-        hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, scale_v, u);
+        hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, vin_fold,
+                           nfold, u);
         hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, u,
                            cpart);
-        hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes,
-                           nullptr, v);
-        stats(v, n, stats_v, scale_v);
+        hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, v,
+                           vfold);
         vin = v;
+        vin_fold = vfold;
     }
     // sigma_1 = |xi v| for the final unit vector v.
-    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, scale_v, u);
-    stats(u, m, stats_u, nullptr);
+    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, vin_fold, nfold,
+                       u);
+    stats(u, m, stats_u);
     if (hipGetLastError() != hipSuccess) return RIKFAD_EHIP;
     double host[6];
     if (hipMemcpyAsync(host, stats_r, sizeof(double) * 2, hipMemcpyDeviceToHost, st) != hipSuccess ||
