@@ -278,7 +278,10 @@ rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n, doub
  * Three passes stream the gradient (statistics, RMS of U, update), so a
  * step moves 28 bytes per fp32 parameter (18 with bf16 x and g; +4 / +2
  * with scale_parameter).  Every call enqueues on `stream` and returns;
- * same error conventions as the R-iKFAD entry points.
+ * same error conventions as the R-iKFAD entry points.  The step's
+ * coefficients depend on t and are passed to the kernels by value, so a
+ * step captured in a HIP graph would replay the same t: capture is not
+ * supported for Adafactor-m.
  * ---------------------------------------------------------------------- */
 typedef struct {
     double h;                /* step size (learning rate), > 0 */
