@@ -237,3 +237,14 @@ def test_adafm_state_equals_rikfad_state():
         gold[f[0]] = dict(adafm=float(f[3]), rikfad=float(f[6]))
     for name in gold:
         assert gold[name]["adafm"] == gold[name]["rikfad"], name
+
+
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_standalone(lang):
+    """include/rikfad.h is a self-contained C header (also usable from C++)."""
+    import subprocess
+    cc = "gcc" if lang == "c" else "g++"
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        r = subprocess.run([cc, "-fsyntax-only", "-Wall", "-Wextra", "-Werror", "-x", lang, h],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
