@@ -59,6 +59,9 @@ EDGE = [
     ("bf16_v4", [S("a", 64, 36, "bf16"), S("b", 200, 776, "bf16")]),
     ("bf16_v1", [S("a", 65, 27, "bf16"), S("b", 1, 33, "bf16")]),
     ("tall", [S("a", 3000, 12), S("b", 2100, 100)]),
+    ("very_wide", [S("a", 40, 50257), S("b", 1, 50257)]),
+    ("many_small", [S(f"t{i}", 3 + i % 5, 5 + i % 7) for i in range(300)]
+                   + [S(f"v{i}", 1, 1 + i % 9) for i in range(300)]),
 ]
 
 

@@ -67,6 +67,9 @@ EDGE = [
     ("bf16_v1", [S("a", 65, 27, "bf16"), S("b", 1, 33, "bf16")]),
     ("tall", [S("a", 3000, 12)]),                            # many stripes, 3 lanes per row
     ("mixed", [S("a", 96, 200), S("b", 1, 200), S("c", 40, 640, "bf16"), S("d", 640, 1, "bf16")]),
+    ("very_wide", [S("a", 40, 50257), S("b", 1, 50257)]),    # 197 column blocks per row
+    ("many_small", [S(f"t{i}", 3 + i % 5, 5 + i % 7) for i in range(300)]
+                   + [S(f"v{i}", 1, 1 + i % 9) for i in range(300)]),
 ]
 
 
