@@ -232,6 +232,18 @@ __device__ __forceinline__ float sum_r(const float *__restrict__ part, int count
     return s;
 }
 
+// v - h g and d v with the split coefficients (h = h + h_lo, d = 1 + dm1):
+// each product is added by a fused multiply-add, so the coefficients'
+// fp32 rounding does not accumulate over steps.
+__device__ __forceinline__ float kick(float v, float g, const Coeffs &k)
+{
+    return __builtin_fmaf(-k.h_lo, g, __builtin_fmaf(-k.h, g, v));
+}
+__device__ __forceinline__ float damp(float v, const Coeffs &k)
+{
+    return __builtin_fmaf(v, k.dm1, v);
+}
+
 // Stage 1 of the row and column sums of a matrix tile, after each wave has
 // walked its rows.  acc[V]: this lane's column sums; myrow: in lane t, the
 // sum of the wave's row r0 + t (t < nr).  Lanes l and l ^ o (o >= L) own the

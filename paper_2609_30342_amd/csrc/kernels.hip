@@ -133,8 +133,8 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
                 const float q = ok ? qv[u][i] : 0.f;
                 const float gg = ok ? gv[i] : 0.f;
                 const float e = exp2f(rate * cv[i]);
-                const float pn = pending ? k.d * (q * e) : q;
-                const float pb = pn - k.h * gg;
+                const float pn = pending ? damp(q * e, k) : q;
+                const float pb = kick(pn, gg, k);
                 xv[i] = xv[i] + k.h * pb;
                 const float p1 = pb * e;
                 qv[u][i] = p1;
@@ -177,11 +177,11 @@ __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__rest
     Io<float, V>::load(xi, fv);
 #pragma unroll
     for (int i = 0; i < V; ++i) {
-        const float pb = pv[i] - k.h * gv[i];
+        const float pb = kick(pv[i], gv[i], k);
         xv[i] = xv[i] + k.h * pb;
         const float p1 = pb * exp2f(k.kh * fv[i]);
         fv[i] = k.a * fv[i] + k.kappa * (p1 * p1);
-        pv[i] = k.d * (p1 * exp2f(k.kh * fv[i]));
+        pv[i] = damp(p1 * exp2f(k.kh * fv[i]), k);
     }
     Io<XT, V>::store(x, xv);
     Io<float, V>::store(p, pv);
@@ -388,7 +388,7 @@ __device__ void apply_matrix(const TensorDesc &td, const Tile &tile, const float
             float qv[V];
             Io<float, V>::load(p + off, qv);
 #pragma unroll
-            for (int i = 0; i < V; ++i) qv[i] = k.d * (qv[i] * exp2f(rate * cv[i]));
+            for (int i = 0; i < V; ++i) qv[i] = damp(qv[i] * exp2f(rate * cv[i]), k);
             Io<float, V>::store(p + off, qv);
         }
     }

@@ -101,12 +101,19 @@ struct FinItem {
 };
 
 // Step coefficients, computed in fp64 on the host and rounded once.
+// h and e^{-gamma h} enter every step of a momentum that can carry the
+// same value for many steps, so their fp32 rounding errors would add up
+// (about 2e-8 relative per step for d at gamma h = 1e-4, amplified where a
+// momentum is a cancelling sum of many kicks).  The kernels therefore apply
+// h as h_hi + h_lo and d as 1 + dm1, each with fused multiply-adds.
 struct Coeffs {
-    float h;           // step size
+    float h;           // step size (h_hi: h rounded to fp32)
+    float h_lo;        // h - h_hi
     float kh;          // -(h/2) log2(e): exp(-(h/2) v) = exp2(kh v)
     float a;           // e^{-alpha h}
     float kappa;       // (1 - e^{-alpha h}) / (mu alpha)
     float d;           // e^{-gamma h}
+    float dm1;         // e^{-gamma h} - 1, from expm1
     float eps;         // eps_stab
 };
 

@@ -104,18 +104,21 @@ rikfad_status check_hparams(const rikfad_hparams *hp, std::string &err)
 
 // App. A Table rows C and D: e^{-alpha h}, (1 - e^{-alpha h})/(mu alpha)
 // evaluated as -expm1(-alpha h)/(mu alpha) (alpha = 0: its limit h/mu),
-// e^{-gamma h}; and -(h/2) log2(e) so that the half-kick is one exp2.
-// All in fp64, rounded once to fp32.
+// e^{-gamma h} (also as expm1(-gamma h)); h as an fp32 pair; and
+// -(h/2) log2(e) so that the half-kick is one exp2.  All in fp64, each
+// rounded once to fp32.
 Coeffs make_coeffs(const rikfad_hparams &hp)
 {
     const double ah = hp.alpha * hp.h;
     Coeffs k;
     k.h = static_cast<float>(hp.h);
+    k.h_lo = static_cast<float>(hp.h - static_cast<double>(k.h));
     k.kh = static_cast<float>(-0.5 * hp.h * 1.44269504088896340736);
     k.a = static_cast<float>(std::exp(-ah));
     k.kappa = static_cast<float>(hp.alpha > 0 ? -std::expm1(-ah) / (hp.mu * hp.alpha)
                                               : hp.h / hp.mu);
     k.d = static_cast<float>(std::exp(-hp.gamma * hp.h));
+    k.dm1 = static_cast<float>(std::expm1(-hp.gamma * hp.h));
     k.eps = static_cast<float>(hp.eps_stab);
     return k;
 }

@@ -1,19 +1,22 @@
 """Shared machinery of the GPU parity tests: run the HIP path (through the C
 ABI binding) and the fp64 oracle on the same seeded inputs and compare.
 
-Error metrics, per tensor:
+Error metrics, per tensor (the tolerance of fp32 state is 1e-5 in both):
   x, p   normwise max relative error max_i |a_i - b_i| / max_i |b_i| <= 1e-5,
-         and element-wise max_i |a_i - b_i| / max(|b_i|, rms(b)) <= 1e-4;
+         and element-wise max_i |a_i - b_i| / max(|b_i|, rms(b)) <= 1e-5;
   R, C   plain max relative error (non-negative, no cancellation; 0/0 = 0)
          <= 1e-5;
   bf16 x the stored value against the oracle's unrounded fp64 update from
          the same bf16 starting point, element-wise with the rms floor,
          <= 4e-3 (rounding to bf16 costs at most 2^-8 relative).
-The element-wise bound is looser because fp32 storage of the momentum alone
-loses about 1e-5 on elements that a random walk of gradients has brought
-back near zero while their own history was several times larger (measured
-with an exact-exponential fp32 emulation on the CPU: 7.5e-6 after 50
-steps of the GPT2-Nano-shaped set; the fp32 kernels reach 1.4e-5).
+The element-wise bound is tight for long runs: fp32 storage of the
+momentum alone loses up to about 1e-5 after 50 steps on elements that a
+cancelling sum of gradient kicks has left much smaller than their own
+history (CPU emulation of the kernels' fp32 arithmetic on the
+GPT2-Nano-shaped set: 1.0e-5 to 1.2e-5; the kernels measure 9.5e-6).  It
+holds because the kernels apply h and e^{-gamma h} as split coefficients
+with fused multiply-adds; with plainly rounded fp32 coefficients the same
+run reaches 1.4e-5.
 """
 from __future__ import annotations
 
@@ -28,7 +31,7 @@ from paper_2609_30342_amd import rikfad as R
 from paper_2609_30342_amd import synth
 
 TOL_F32 = 1e-5
-TOL_F32_ELEM = 1e-4
+TOL_F32_ELEM = 1e-5
 TOL_BF16 = 4e-3
 
 

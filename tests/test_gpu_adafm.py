@@ -4,7 +4,7 @@ Section 3 and App. "Hyperparameters") through the C ABI against the fp64
 oracle, on the same seeded synthetic workloads as the R-iKFAD tests.
 
 Tolerances are those of the R-iKFAD parity tests: x and the first moment M
-normwise 1e-5 (element-wise 1e-4 with the rms floor), the factors R, C and
+normwise and element-wise (with the rms floor) 1e-5, the factors R, C and
 the unfactored second moment of vectors plain relative 1e-5, bf16 x against
 the oracle's unrounded update 4e-3.  Every case prints its name first.
 """
