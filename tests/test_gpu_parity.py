@@ -116,6 +116,83 @@ def test_empty_parameter_list_is_a_noop():
     R.rikfad_destroy(ctx)
 
 
+def test_tensor_beyond_2_31_elements():
+    """One 50000 x 50000 bf16 tensor (2.5e9 elements: element offsets past
+    2^31) with the rank-1 power-of-two gradient g_ij = a_i b_j (exact in
+    bf16), x = p = r = c = 0, two steps with the same gradient.  The Table's
+    step has closed forms here.  Step 1: xi~ = 0, P^(1) = -h g, X = -h^2 g,
+    R_i = kappa h^2 a_i^2 sum_j b_j^2, C_j = kappa h^2 b_j^2 sum_i a_i^2.
+    Step 2: E_ij = exp(-(h/2) R_i C_j / (1^T R + eps)), P^(B) = P^(1) E - h g,
+    X += h P^(B), P^(1) = P^(B) E, and the factors from its row and column
+    sums.  Checked on sampled elements (half in rows past 2^31 / n) and on
+    sampled rows of R and columns of C."""
+    m = n = 50000
+    h, alpha, mu, eps = 0.05, 0.1, 1e-4, 1e-8
+    log(f"[case] {m}x{n} bf16 tensor ({m * n} elements)")
+    kappa = -np.expm1(-alpha * h) / (mu * alpha)
+    arel = np.exp(-alpha * h)
+    ia, jb = np.arange(m), np.arange(n)
+    a = 2.0 ** (ia % 3 - 1)
+    b = 2.0 ** (jb % 5 - 2)
+    dev = "cuda:0"
+    x = torch.zeros((m, n), dtype=torch.bfloat16, device=dev)
+    g = (torch.from_numpy(a.astype(np.float32)).to(dev)[:, None]
+         * torch.from_numpy(b.astype(np.float32)).to(dev)[None, :]).to(torch.bfloat16)
+    opt = R.RIKFAD([x], [g], h=h, gamma=0.0, alpha=alpha, mu=mu, eps_stab=eps)
+    p, r, c = opt.state[0]
+    rng = np.random.default_rng(31)
+    rows = np.concatenate([rng.integers(0, m, 24), rng.integers(43000, m, 24)])
+    cols = rng.integers(0, n, 48)
+    ri, cj = torch.from_numpy(rows).to(dev), torch.from_numpy(cols).to(dev)
+
+    def sample(t):
+        return t[ri][:, cj].to(torch.float64).cpu().numpy()
+
+    errs = {}
+
+    def check(name, got, want, floor, tol):
+        e = float(np.max(np.abs(got - want) / np.maximum(np.abs(want), floor)))
+        errs[name] = e
+        assert e <= tol, (name, e, errs)
+
+    G = a[rows][:, None] * b[cols][None, :]
+    # step 1
+    opt.step()
+    torch.cuda.synchronize()
+    x1 = sample(x)
+    P1 = -h * G
+    check("x1", x1, -h * h * G, np.sqrt(np.mean((h * h * G) ** 2)), 4e-3)
+    check("p1", sample(p), P1, np.sqrt(np.mean(P1 ** 2)), 1e-5)
+    R1 = kappa * h * h * a ** 2 * np.sum(b ** 2)
+    C1 = kappa * h * h * b ** 2 * np.sum(a ** 2)
+    check("r1", r[ri].double().cpu().numpy(), R1[rows], 0.0, 1e-5)
+    check("c1", c[cj].double().cpu().numpy(), C1[cols], 0.0, 1e-5)
+    # step 2 (same gradient): closed forms from the step-1 factors
+    opt.step()
+    torch.cuda.synchronize()
+    S1 = np.sum(R1)
+
+    def E(i, j):
+        return np.exp(-0.5 * h * np.outer(R1[i], C1[j]) / (S1 + eps))
+
+    Es = E(rows, cols)
+    PB = P1 * Es - h * G
+    check("x2", sample(x), x1 + h * PB, np.sqrt(np.mean((h * PB) ** 2)), 4e-3)
+    P2 = PB * Es
+    check("p2", sample(p), P2, np.sqrt(np.mean(P2 ** 2)), 1e-5)
+    # factors: full row sums for the sampled rows, column sums for the sampled columns
+    Er = E(rows, jb)
+    rowsq = np.sum((h * a[rows][:, None] * b[None, :] * (Er + 1.0) * Er) ** 2, axis=1)
+    Ec = E(ia, cols)
+    colsq = np.sum((h * a[:, None] * b[cols][None, :] * (Ec + 1.0) * Ec) ** 2, axis=0)
+    check("r2", r[ri].double().cpu().numpy(), arel * R1[rows] + kappa * rowsq, 0.0, 1e-5)
+    check("c2", c[cj].double().cpu().numpy(), arel * C1[cols] + kappa * colsq, 0.0, 1e-5)
+    log(f"[parity] 50000x50000 errs={ {k: f'{v:.2e}' for k, v in errs.items()} }")
+    opt.close()
+    del x, g, p, r, c
+    torch.cuda.empty_cache()
+
+
 # ------------------------------------------------------ model-shaped sets
 
 @pytest.mark.parametrize("variant", ["base", "gamma", "eps0"])
