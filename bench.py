@@ -100,10 +100,10 @@ def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0):
                 apply_ms=k3 / n, info=info, nonfinite=nonfinite)
 
 
-def time_ikfad(specs, hp, steps, warmup, seed=0):
+def time_ikfad(specs, hp, steps, warmup, seed=0, dtype="fp32"):
     import torch
     from paper_2609_30342_amd import rikfad as R
-    xs, gs = build_workload(specs, "fp32", seed, torch.device("cuda:0"))
+    xs, gs = build_workload(specs, dtype, seed, torch.device("cuda:0"))
     ik = R.IKFAD(xs, gs, h=hp["h"], gamma=hp["gamma"], alpha=hp["alpha"], mu=hp["mu"])
     for _ in range(warmup):
         ik.step()
@@ -245,19 +245,31 @@ def cpu_baseline(specs, hp, budget_s):
     grads = [wl.grad(i, 0).astype(np.float64) for i in range(len(sample))]
     threads = len(os.sched_getaffinity(0))
     ohp = O.HParams(**hp)
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        O.step_list(ts, grads, ohp, threads=threads)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
+
+    def rate(nthreads, seconds):
+        n, t0 = 0, time.perf_counter()
+        while True:
+            O.step_list(ts, grads, ohp, threads=nthreads)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                return n, el
+
     elems = sum(s.numel for s in sample)
+    n, el = rate(threads, budget_s)
+    n1, el1 = rate(1, max(1.0, budget_s / 6))
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")),
+                         "")
+    except OSError:
+        pass
     return {"value": elems * n / el, "unit": "params/s", "cores": threads, "kind": "oracle",
+            "single_thread_value": elems * n1 / el1, "cpu_model": model,
             "sample": f"fp64 oracle, {n} steps over wpe + block 0 of the GPT2-S set "
                       f"({elems} params, {len(sample)} tensors), OpenMP over tensors, "
-                      f"{el:.1f} s"}
+                      f"{el:.1f} s; single thread: {n1} steps in {el1:.1f} s"}
 
 
 def main():
@@ -343,11 +355,11 @@ def main():
         tp = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup, two_pass=True)
         var["rikfad_two_pass"] = {"ms_per_step": tp["ms_per_step"],
                                   "params_per_s": N / (tp["ms_per_step"] * 1e-3)}
-        if args.dtype == "fp32":
-            ik_ms = time_ikfad(specs, hp, args.steps, args.warmup)
-            var["ikfad_full_fp32"] = {"ms_per_step": ik_ms, "params_per_s": N / (ik_ms * 1e-3),
-                                      "hbm_gbps": 28.0 * N / (ik_ms * 1e-3) / 1e9,
-                                      "state_bytes": info["ikfad_state_bytes"]}
+        for idt, per in (("fp32", 28.0), ("bf16", 22.0)):
+            ik_ms = time_ikfad(synth.gpt2_small(idt), hp, args.steps, args.warmup, dtype=idt)
+            var[f"ikfad_full_{idt}"] = {"ms_per_step": ik_ms, "params_per_s": N / (ik_ms * 1e-3),
+                                        "hbm_gbps": per * N / (ik_ms * 1e-3) / 1e9,
+                                        "state_bytes": info["ikfad_state_bytes"]}
         var["adafm_fp32"] = time_adafm(synth.gpt2_small("fp32"), "fp32", args.steps,
                                        args.warmup, h=1e-3, beta1=0.9)
         var["adafm_bf16"] = time_adafm(synth.gpt2_small("bf16"), "bf16", args.steps,
