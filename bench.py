@@ -287,7 +287,7 @@ def main():
                          "known traffic for scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
+        print(f"bench.py: the step runs on one GPU (no multi-GPU path); --gpus {args.gpus} is not "
               "supported", file=sys.stderr)
         return 2
 
