@@ -15,7 +15,8 @@
 // sigma_1 comes from power iteration on xi^T xi started at C / |C| (xi >= 0,
 // so the leading singular vectors are non-negative), normalised on the GPU:
 // the column fold also writes per-workgroup squared-norm partials, from
-// which every wave of the next row pass derives the same scale.
+// which every wave of the next row pass derives the same scale.  For
+// n <= 1024 an iteration reads xi once (u = xi v and xi^T u in one pass).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -83,6 +84,78 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
     }
     s = wave_sum(s);
     if (lane == 0) gp(out)[row] = w ? s * scale : s;
+}
+
+// One power-iteration pass over xi for n <= 64 * NC, reading xi once: a
+// workgroup takes kPowRows rows, each wave a quarter of them in order.  Lane l holds columns l, l + 64, ... of a row in registers; the wave
+// forms u_i = sum_j xi[i, j] v[j] scale (lanes in column order, then the
+// butterfly) and adds xi[i, j] u_i to its column accumulators, rows in
+// order.  The waves' column sums are added in wave order into the
+// workgroup's row of part (folded by col_fold_kernel).
+constexpr int kPowRows = 128;      // rows per workgroup
+constexpr int kPowRing = 3;        // row loads in flight per wave
+
+template <int NC>
+__global__ __launch_bounds__(kT) void power_step_kernel(const float *__restrict__ xi, int64_t m,
+                                                        int64_t n, const double *__restrict__ v,
+                                                        const double *__restrict__ vparts,
+                                                        int64_t nvparts, double *__restrict__ part)
+{
+    __shared__ double l[kT / 64][64 * NC];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const double scale = inv_norm(vparts, nvparts);
+    double wv[NC], acc[NC];
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+        const int64_t j = lane + 64 * k;
+        wv[k] = j < n ? gp(v)[j] * scale : 0.0;
+        acc[k] = 0.0;
+    }
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kPowRows + wave * (kPowRows / 4);
+    const int64_t r1 = r0 + kPowRows / 4 < m ? r0 + kPowRows / 4 : m;
+    // A ring of kPowRing rows per wave: the loads of row i + kPowRing go out
+    // before row i is reduced, so the butterflies overlap the loads.
+    float ring[kPowRing][NC];
+#pragma unroll
+    for (int q = 0; q < kPowRing; ++q) {
+#pragma unroll
+        for (int k = 0; k < NC; ++k) {
+            const int64_t j = lane + 64 * k;
+            ring[q][k] = (j < n && r0 + q < r1) ? gp(xi)[(r0 + q) * n + j] : 0.f;
+        }
+    }
+    for (int64_t i0 = r0; i0 < r1; i0 += kPowRing) {
+#pragma unroll
+        for (int q = 0; q < kPowRing; ++q) {
+            const int64_t i = i0 + q;
+            float a[NC];
+#pragma unroll
+            for (int k = 0; k < NC; ++k) a[k] = ring[q][k];
+            const int64_t nx = i + kPowRing;
+#pragma unroll
+            for (int k = 0; k < NC; ++k) {
+                const int64_t j = lane + 64 * k;
+                ring[q][k] = (j < n && nx < r1) ? gp(xi)[nx * n + j] : 0.f;
+            }
+            double su = 0.0;
+#pragma unroll
+            for (int k = 0; k < NC; ++k) su += static_cast<double>(a[k]) * wv[k];
+            su = wave_sum(su);
+            if (i < r1) {
+#pragma unroll
+                for (int k = 0; k < NC; ++k) acc[k] += static_cast<double>(a[k]) * su;
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < NC; ++k) l[wave][lane + 64 * k] = acc[k];
+    __syncthreads();
+    for (int64_t j = threadIdx.x; j < n; j += kT) {
+        double s = l[0][j];
+#pragma unroll
+        for (int w = 1; w < kT / 64; ++w) s += l[w][j];
+        gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
+    }
 }
 
 // part[s, j] = sum over rows i of stripe s of xi[i, j] * (w ? w[i] : 1).
@@ -307,12 +380,16 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     // workspace (doubles): r m, c n, u m, v n, column partials nstripes*n,
     // error partials 2*nerr, fold partials 2*nfold (C) and 2*nfold (v),
     // statistics partials 2*nstat, results 2 (R), 2 (u), 2 (errors)
-    const int64_t words = m + n + m + n + nstripes * n + 2 * nerr + 4 * nfold + 2 * nstat + 6;
+    // n <= 1024: one pass over xi per power iteration (power_step_kernel)
+    const int nc = n <= 256 ? 4 : n <= 512 ? 8 : n <= 768 ? 12 : n <= 1024 ? 16 : 0;
+    const int64_t nblk = (m + kPowRows - 1) / kPowRows;
+    const int64_t nparts = nc && nblk > nstripes ? nblk : nstripes;
+    const int64_t words = m + n + m + n + nparts * n + 2 * nerr + 4 * nfold + 2 * nstat + 6;
     DevBuf buf;
     if (hipMalloc(&buf.p, sizeof(double) * static_cast<size_t>(words)) != hipSuccess)
         return RIKFAD_ENOMEM;
     double *r = static_cast<double *>(buf.p), *c = r + m, *u = c + n, *v = u + m;
-    double *cpart = v + n, *epart = cpart + nstripes * n, *cfold = epart + 2 * nerr;
+    double *cpart = v + n, *epart = cpart + nparts * n, *cfold = epart + 2 * nerr;
     double *vfold = cfold + 2 * nfold, *spart = vfold + 2 * nfold;
     double *stats_r = spart + 2 * nstat, *stats_u = stats_r + 2, *err = stats_u + 2;
     const dim3 rows_grid(static_cast<uint32_t>((m + kT / 64 - 1) / (kT / 64)));
@@ -340,13 +417,31 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     // each row pass normalises its input from the fold partials of the last
     // column pass.
     const double *vin = c, *vin_fold = cfold;
+    const dim3 pow_grid(static_cast<uint32_t>(nblk));
     for (int it = 0; it < power_iters; ++it) {
-        hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, vin_fold,
-                           nfold, u);
-        hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, u,
-                           cpart);
-        hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, v,
-                           vfold);
+        if (nc) {
+            if (nc == 4)
+                hipLaunchKernelGGL(power_step_kernel<4>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
+                                   vin_fold, nfold, cpart);
+            else if (nc == 8)
+                hipLaunchKernelGGL(power_step_kernel<8>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
+                                   vin_fold, nfold, cpart);
+            else if (nc == 12)
+                hipLaunchKernelGGL(power_step_kernel<12>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
+                                   vin_fold, nfold, cpart);
+            else
+                hipLaunchKernelGGL(power_step_kernel<16>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
+                                   vin_fold, nfold, cpart);
+            hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nblk, v,
+                               vfold);
+        } else {
+            hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin,
+                               vin_fold, nfold, u);
+            hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, u,
+                               cpart);
+            hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, v,
+                               vfold);
+        }
         vin = v;
         vin_fold = vfold;
     }
