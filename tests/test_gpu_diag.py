@@ -40,6 +40,8 @@ CASES = [
     ("mixture3_300x520", lambda: _mixture(300, 520, 3, 4), 1e-8),
     ("mixture5_4097x64", lambda: _mixture(4097, 64, 5, 5), 0.0),
     ("single_row", lambda: _mixture(1, 300, 1, 6), 0.0),
+    ("mixture2_700x1000", lambda: _mixture(700, 1000, 2, 7), 1e-8),    # widest one-pass rows
+    ("mixture2_300x1025", lambda: _mixture(300, 1025, 2, 8), 1e-8),    # two-pass iteration
 ]
 
 
