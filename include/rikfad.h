@@ -233,9 +233,10 @@ void ikfad_destroy(ikfad_ctx *ctx);
  * Eckart-Young floor sqrt(1 - sigma_1^2 / |xi|_F^2) and the stable rank
  * |xi|_F^2 / sigma_1^2.  All reductions are fp64 in a fixed order.
  * Blocking (waits for `stream`); allocates and frees a temporary device
- * workspace of 8 (2 m + 2 n + n ceil(m / s)) bytes plus a little, where the
- * column-sum stripe height s is a power of two in [16, 1024] (larger only
- * for m above 2^20).  m, n < 2^31; EINVAL on bad arguments, ENOMEM if the
+ * workspace of 8 (2 m + 2 n + n max(ceil(m / s), ceil(m / 128))) bytes plus
+ * a little, where the column-sum stripe height s is a power of two in
+ * [16, 1024] (larger only for m above 2^20).  For n <= 1024 a power
+ * iteration reads xi once, otherwise twice.  m, n < 2^31; EINVAL on bad arguments, ENOMEM if the
  * workspace cannot be allocated, EHIP on a launch or copy failure.
  * ---------------------------------------------------------------------- */
 typedef struct {
