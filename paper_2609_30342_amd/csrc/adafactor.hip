@@ -240,6 +240,8 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
         flat_tile(tile, op);
         u2 = op.u2;
         x2 = op.x2;
+    } else if (V > 1 && tile.vec == 1) {
+        stats_matrix<XT, 1, X2>(td, g, tile, ws, k, lds, x2);
     } else {
         stats_matrix<XT, V, X2>(td, g, tile, ws, k, lds, x2);
     }
@@ -252,22 +254,15 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
 
 // ---------------------------------------------------------------- pass 2
 
+// Sum of U^2 over one matrix tile (this lane's share).
 template <typename XT, int V>
-__global__ __launch_bounds__(kStreamThreads) void adafm_rms_kernel(
-    const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
-    const Tile *__restrict__ tiles, int64_t tile0, const float *__restrict__ ws,
-    float *__restrict__ tilepart)
+__device__ float rms_matrix(const TensorDesc &td, const XT *__restrict__ g, const Tile &tile,
+                            const float *__restrict__ ws)
 {
-    __shared__ float red[2 * kStreamWaves];
-    const int64_t ti = tile0 + blockIdx.x;
-    const Tile tile = tiles[ti];
-    if (tile.kind == KIND_VECTOR) return;   // vector sums are complete after pass 1
-    const TensorDesc td = tensors[tile.tensor];
-    const XT *__restrict__ g = static_cast<const XT *>(grads[tile.tensor]);
     const Lanes t = lanes_of<V>(tile);
     float fc[V];
     const float myfr = tile_factors<V>(td, t, ws, fc);
-    float u2 = 0.f, zero = 0.f;
+    float u2 = 0.f;
     for (int ld0 = 0; ld0 < t.nld; ld0 += kBatch) {
         typename Raw<XT, V>::type gr[kBatch];
 #pragma unroll
@@ -286,6 +281,24 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_rms_kernel(
             }
         }
     }
+    return u2;
+}
+
+template <typename XT, int V>
+__global__ __launch_bounds__(kStreamThreads) void adafm_rms_kernel(
+    const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
+    const Tile *__restrict__ tiles, int64_t tile0, const float *__restrict__ ws,
+    float *__restrict__ tilepart)
+{
+    __shared__ float red[2 * kStreamWaves];
+    const int64_t ti = tile0 + blockIdx.x;
+    const Tile tile = tiles[ti];
+    if (tile.kind == KIND_VECTOR) return;   // vector sums are complete after pass 1
+    const TensorDesc td = tensors[tile.tensor];
+    const XT *__restrict__ g = static_cast<const XT *>(grads[tile.tensor]);
+    float u2 = V > 1 && tile.vec == 1 ? rms_matrix<XT, 1>(td, g, tile, ws)
+                                      : rms_matrix<XT, V>(td, g, tile, ws);
+    float zero = 0.f;
     block_sum2<kStreamWaves>(u2, zero, red);
     if (threadIdx.x == 0) gmem(tilepart)[2 * ti] = u2;
 }
@@ -402,18 +415,19 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_update_kernel(
         flat_tile(tile, op);
         return;
     }
-    update_matrix<XT, V>(td, g, tile, ws, s, k);
+    if (V > 1 && tile.vec == 1) update_matrix<XT, 1>(td, g, tile, ws, s, k);
+    else update_matrix<XT, V>(td, g, tile, ws, s, k);
 }
 
-// Kernel instantiation for a tile group's (storage type, access width);
-// nullptr for a combination the planner does not produce.
+// Kernel instantiation for a tile group's (storage type, width); the 4-wide
+// one also serves the group's one-column tiles.  nullptr for a combination
+// the planner does not produce.
 template <typename F, typename Pick>
 F pick(const TileGroup &gr, Pick p)
 {
     if (gr.dtype == DT_F32) return gr.vec == 4 ? p.template get<float, 4>()
                                 : gr.vec == 1 ? p.template get<float, 1>() : nullptr;
-    return gr.vec == 8 ? p.template get<uint16_t, 8>()
-         : gr.vec == 4 ? p.template get<uint16_t, 4>()
+    return gr.vec == 4 ? p.template get<uint16_t, 4>()
          : gr.vec == 1 ? p.template get<uint16_t, 1>() : nullptr;
 }
 

@@ -26,12 +26,6 @@
 #include "kernels.hpp"
 #include "layout.hpp"
 
-// RK_PERSIST = k > 0: the streaming kernel runs a grid of k workgroups per
-// compute unit looping over the tiles (measured slower; kept as a switch).
-#ifndef RK_PERSIST
-#define RK_PERSIST 0
-#endif
-
 namespace rk {
 
 // kh * R_i / (1^T R + eps), or 0 where the denominator vanishes (the
@@ -230,19 +224,6 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
     Coeffs k, int pending)
 {
     __shared__ float lds[kStreamWaves * kWave * V];
-#if RK_PERSIST
-    for (int64_t t = blockIdx.x; t < ntile; t += gridDim.x) {
-        const Tile tile = tiles[tile0 + t];
-        const TensorDesc td = tensors[tile.tensor];
-        const void *g = grads[tile.tensor];
-        if (tile.kind == KIND_VECTOR) {
-            elementwise_tile<XT, kStreamThreads>(td, g, tile, k);
-        } else {
-            stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
-        }
-        __syncthreads();
-    }
-#else
     const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
@@ -250,8 +231,12 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
         elementwise_tile<XT, kStreamThreads>(td, g, tile, k);
         return;
     }
-    stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
-#endif
+    // Tensors whose rows break 16-byte alignment ride along in the same
+    // launch on the one-column path (fewer registers than the wide path).
+    if (V > 1 && tile.vec == 1)
+        stream_matrix<XT, 1>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
+    else
+        stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
 }
 
 // Finalisation (C.2 / C.3 stage 2).  Row items: thread t owns row start+t,
@@ -402,7 +387,8 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_apply_kernel(
     const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     if (tile.kind != KIND_MATRIX) return;
-    apply_matrix<V>(td, tile, ws, k);
+    if (V > 1 && tile.vec == 1) apply_matrix<1>(td, tile, ws, k);
+    else apply_matrix<V>(td, tile, ws, k);
 }
 
 // Full-tensor iKFAD: every tile is an element range with its own friction.
@@ -474,12 +460,7 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
-#if RK_PERSIST
-        const int64_t cap = int64_t(256) * RK_PERSIST;
-        const dim3 grid(static_cast<uint32_t>(gr.count < cap ? gr.count : cap)), block(kStreamThreads);
-#else
         const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
-#endif
 #define RK_LAUNCH(XT, V)                                                                     \
     hipLaunchKernelGGL((rikfad_stream_kernel<XT, V>), grid, block, 0, stream, tensors, grads, \
                        tiles, gr.begin, gr.count, ws, k, pending)
@@ -487,8 +468,7 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
             if (gr.vec == 4) RK_LAUNCH(float, 4);
             else RK_LAUNCH(float, 1);
         } else {
-            if (gr.vec == 8) RK_LAUNCH(uint16_t, 8);
-            else if (gr.vec == 4) RK_LAUNCH(uint16_t, 4);
+            if (gr.vec == 4) RK_LAUNCH(uint16_t, 4);
             else RK_LAUNCH(uint16_t, 1);
         }
 #undef RK_LAUNCH
@@ -515,10 +495,7 @@ hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const Tile
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
-        if (gr.vec == 8)
-            hipLaunchKernelGGL(rikfad_apply_kernel<8>, grid, block, 0, stream, tensors, tiles,
-                               gr.begin, ws, k);
-        else if (gr.vec == 4)
+        if (gr.vec == 4)
             hipLaunchKernelGGL(rikfad_apply_kernel<4>, grid, block, 0, stream, tensors, tiles,
                                gr.begin, ws, k);
         else

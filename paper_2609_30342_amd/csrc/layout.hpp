@@ -76,8 +76,10 @@ struct Tile {
 };
 
 // A contiguous range of the tile table served by one launch of the
-// streaming kernel instantiated for the (dtype, vec) of its matrix tiles.
-// Vector tiles of the same dtype are appended to one group of that dtype.
+// streaming kernel: the matrix tiles of one storage type (4-wide ones
+// first, then one-column ones, which the 4-wide instantiation also serves),
+// then that type's vector tiles.  vec (4, or 1 when the type has no 4-wide
+// matrix tile) selects the kernel instantiation.
 struct TileGroup {
     int32_t dtype;
     int32_t vec;

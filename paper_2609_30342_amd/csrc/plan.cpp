@@ -23,12 +23,6 @@ int32_t matrix_vec(const rikfad_tensor &t)
 {
     if (t.dtype == RIKFAD_FP32)
         return (t.n % 4 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) ? 4 : 1;
-#ifndef RK_BF16_MAXVEC
-#define RK_BF16_MAXVEC 4
-#endif
-    if (RK_BF16_MAXVEC >= 8 && t.n % 8 == 0 && aligned(t.x, 16) && aligned(t.g, 16) &&
-        aligned(t.p, 16))
-        return 8;
     if (t.n % 4 == 0 && aligned(t.x, 8) && aligned(t.g, 8) && aligned(t.p, 16)) return 4;
     return 1;
 }
@@ -157,11 +151,11 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     int64_t ws = 0;
     pl.tensors.resize(static_cast<size_t>(count));
     pl.grads.resize(static_cast<size_t>(count));
-    // Matrix tiles by launch class (fp32 v4, fp32 v1, bf16 v8, bf16 v4,
-    // bf16 v1); vector tiles by dtype.
-    const int32_t class_dtype[5] = {DT_F32, DT_F32, DT_BF16, DT_BF16, DT_BF16};
-    const int32_t class_vec[5] = {4, 1, 8, 4, 1};
-    std::vector<Tile> mat_tiles[5];
+    // Matrix tiles by class (fp32 v4, fp32 v1, bf16 v4, bf16 v1); vector
+    // tiles by dtype.
+    const int32_t class_dtype[4] = {DT_F32, DT_F32, DT_BF16, DT_BF16};
+    const int32_t class_vec[4] = {4, 1, 4, 1};
+    std::vector<Tile> mat_tiles[4];
     std::vector<Tile> vec_tiles[2];
     std::vector<FinItem> col_items, fold_items;
     for (int64_t i = 0; i < count; ++i) {
@@ -279,26 +273,20 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                                      static_cast<int32_t>(T.n - j0 < kWave ? T.n - j0 : kWave), q,
                                      0});
     }
-    bool vec_placed[2] = {false, false};
-    for (int cls = 0; cls < 5; ++cls) {
-        if (mat_tiles[cls].empty()) continue;
-        const int dt = class_dtype[cls] == DT_F32 ? 0 : 1;
-        TileGroup gr{class_dtype[cls], class_vec[cls], static_cast<int64_t>(pl.tiles.size()), 0};
-        pl.tiles.insert(pl.tiles.end(), mat_tiles[cls].begin(), mat_tiles[cls].end());
-        pl.matrix_tiles += static_cast<int64_t>(mat_tiles[cls].size());
-        if (!vec_placed[dt]) {
-            pl.tiles.insert(pl.tiles.end(), vec_tiles[dt].begin(), vec_tiles[dt].end());
-            vec_placed[dt] = true;
-        }
-        gr.count = static_cast<int64_t>(pl.tiles.size()) - gr.begin;
-        pl.groups.push_back(gr);
-    }
+    // One streaming launch per storage type: its 4-wide matrix tiles, then
+    // its one-column matrix tiles (served by the same launch), then its
+    // vector tiles.  The group's width selects the kernel instantiation.
     for (int dt = 0; dt < 2; ++dt) {
-        if (vec_placed[dt] || vec_tiles[dt].empty()) continue;
-        TileGroup gr{dt == 0 ? DT_F32 : DT_BF16, 1, static_cast<int64_t>(pl.tiles.size()),
-                     static_cast<int64_t>(vec_tiles[dt].size())};
+        const int wide = 2 * dt, narrow = 2 * dt + 1;
+        TileGroup gr{dt == 0 ? DT_F32 : DT_BF16, mat_tiles[wide].empty() ? 1 : 4,
+                     static_cast<int64_t>(pl.tiles.size()), 0};
+        for (int cls : {wide, narrow}) {
+            pl.tiles.insert(pl.tiles.end(), mat_tiles[cls].begin(), mat_tiles[cls].end());
+            pl.matrix_tiles += static_cast<int64_t>(mat_tiles[cls].size());
+        }
         pl.tiles.insert(pl.tiles.end(), vec_tiles[dt].begin(), vec_tiles[dt].end());
-        pl.groups.push_back(gr);
+        gr.count = static_cast<int64_t>(pl.tiles.size()) - gr.begin;
+        if (gr.count > 0) pl.groups.push_back(gr);
     }
     pl.row_items = static_cast<int64_t>(pl.fin.size());
     pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());

@@ -14,7 +14,7 @@ namespace rk {
 struct Plan {
     std::vector<TensorDesc> tensors;
     std::vector<const void *> grads;
-    std::vector<Tile> tiles;          // grouped by (dtype, vec); see TileGroup
+    std::vector<Tile> tiles;          // grouped by storage type; see TileGroup
     std::vector<TileGroup> groups;    // one streaming launch each
     int64_t matrix_tiles = 0;
     std::vector<FinItem> fin;         // row items, column items, then fold items

@@ -146,15 +146,23 @@ static void check_plan(const Plan &pl, int64_t count)
             CHECK(disjoint || regions[a].second == 0 || regions[b].second == 0, "regions overlap");
         }
     }
-    // groups partition the tile table; matrix tiles match their group class
+    // groups partition the tile table, one group per storage type; a
+    // group's matrix tiles are its own width or one-column (served by the
+    // same instantiation), and a one-column group holds no wider tile
     int64_t covered = 0;
+    bool seen[2] = {false, false};
     for (const TileGroup &g : pl.groups) {
         CHECK(g.begin == covered, "groups not contiguous");
+        CHECK(g.count > 0, "empty group");
+        CHECK(g.vec == 4 || g.vec == 1, "group width");
+        const int dt = g.dtype == DT_F32 ? 0 : 1;
+        CHECK(!seen[dt], "two groups of one storage type");
+        seen[dt] = true;
         covered += g.count;
         for (int64_t t = g.begin; t < g.begin + g.count; ++t) {
             const Tile &tl = pl.tiles[static_cast<size_t>(t)];
             CHECK(tl.dtype == g.dtype, "tile dtype vs group");
-            if (tl.kind == KIND_MATRIX) CHECK(tl.vec == g.vec, "tile vec vs group");
+            if (tl.kind == KIND_MATRIX) CHECK(tl.vec == g.vec || tl.vec == 1, "tile vec vs group");
         }
     }
     CHECK(covered == static_cast<int64_t>(pl.tiles.size()), "groups do not cover tiles");
