@@ -50,16 +50,24 @@ def measured_traffic(dtype):
     return None if entry is None else entry.get("bytes_per_launch")
 
 
-def build_workload(specs, dtype, seed, device):
-    """dtype None: each tensor in its own spec's storage type."""
+def build_workload(specs, dtype, seed, device, scales="lognormal"):
+    """dtype None: each tensor in its own spec's storage type.  scales:
+    "lognormal" row and column scales LogNormal(0, 0.5); "student_t" row
+    scales |T| with T ~ Student-t(3) (drawn as z0 / sqrt((z1^2 + z2^2 +
+    z3^2) / 3)), column scales 1."""
     import torch
     gen = torch.Generator(device=device).manual_seed(seed)
     xs, gs = [], []
     for sp in specs:
         dt = torch.bfloat16 if (dtype or sp.dtype) == "bf16" else torch.float32
         x = (torch.randn((sp.m, sp.n), generator=gen, device=device) * 0.02).to(dt)
-        s = torch.exp(0.5 * torch.randn(sp.m, generator=gen, device=device))
-        t = torch.exp(0.5 * torch.randn(sp.n, generator=gen, device=device))
+        if scales == "student_t":
+            z = torch.randn((4, sp.m), generator=gen, device=device)
+            s = (z[0] / torch.sqrt((z[1:] ** 2).sum(0) / 3.0)).abs()
+            t = torch.ones(sp.n, device=device)
+        else:
+            s = torch.exp(0.5 * torch.randn(sp.m, generator=gen, device=device))
+            t = torch.exp(0.5 * torch.randn(sp.n, generator=gen, device=device))
         g = (torch.randn((sp.m, sp.n), generator=gen, device=device) * s[:, None]
              * t[None, :]).to(dt)
         xs.append(x.contiguous())
@@ -67,11 +75,11 @@ def build_workload(specs, dtype, seed, device):
     return xs, gs
 
 
-def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0):
+def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0, scales="lognormal"):
     import torch
     from paper_2609_30342_amd import rikfad as R
     dev = torch.device("cuda:0")
-    xs, gs = build_workload(specs, dtype, seed, dev)
+    xs, gs = build_workload(specs, dtype, seed, dev, scales)
     opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
     info = opt.query()
     for _ in range(warmup):
@@ -366,6 +374,16 @@ def main():
                                        args.warmup, h=1e-3, beta1=0.9)
         var["adafm_bf16"] = time_adafm(synth.gpt2_small("bf16"), "bf16", args.steps,
                                        args.warmup, h=1e-3, beta1=0.9)
+        big = synth.distilbert_stress()
+        rb = time_rikfad(big, None, hp, 10, 3, scales="student_t")
+        nb = sum(sp.numel for sp in big)
+        var["distilbert_plus_32_large_bf16"] = {
+            "params": nb, "ms_per_step": rb["ms_per_step"],
+            "params_per_s": nb / (rb["ms_per_step"] * 1e-3),
+            "min_bytes_per_step": rb["info"]["min_bytes_per_step"],
+            "hbm_gbps_step": rb["info"]["min_bytes_per_step"] / (rb["ms_per_step"] * 1e-3) / 1e9,
+            "stream_ms": rb["stream_ms"],
+            "stream_gbps": rb["info"]["stream_min_bytes"] / (rb["stream_ms"] * 1e-3) / 1e9}
         var["probe_3r2w_gbps"] = time_probe(N)
         var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {

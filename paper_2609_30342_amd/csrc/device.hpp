@@ -26,31 +26,19 @@ __device__ __forceinline__ RK_GLOBAL T *gmem(T *q)
     return (RK_GLOBAL T *)q;
 }
 
-// Streams are read and written exactly once per step.  With RK_NT the
-// accesses carry the non-temporal hint so they do not displace the small,
-// reused data (factors, partial sums, tables) from the caches.
-#ifndef RK_NT
-#define RK_NT 1
-#endif
-
+// Streams are read and written exactly once per step: the accesses carry
+// the non-temporal hint so they do not displace the small, reused data
+// (factors, partial sums, tables) from the caches.
 template <typename T>
 __device__ __forceinline__ T ldg(const T *q)
 {
-#if RK_NT
     return __builtin_nontemporal_load(gmem(q));
-#else
-    return *gmem(q);
-#endif
 }
 
 template <typename T>
 __device__ __forceinline__ void stg(T *q, T v)
 {
-#if RK_NT
     __builtin_nontemporal_store(v, gmem(q));
-#else
-    *gmem(q) = v;
-#endif
 }
 
 // Native clang vectors (the HIP float4 class cannot bind to an

@@ -33,6 +33,7 @@ constexpr int kMaxRowsPerWave = 64;             // lane t keeps row t's partial 
 constexpr int kBlockLanes = RK_BLOCK_LANES;     // lanes per row of a full column block
 constexpr int kRowsPerWave = RK_ROWS_PER_WAVE;  // rows per wave of a matrix tile
 constexpr int kChunkRows = kThreads;            // rows per finalisation item
+constexpr int kSmallSetTiles = 256;             // compute units of the chip
 constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kVecIters
 
 enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };

@@ -123,6 +123,36 @@ bool grad_fits(const void *g, int32_t dtype, int32_t vec)
     return aligned(g, static_cast<uintptr_t>(esize(dtype)) * static_cast<uintptr_t>(vec));
 }
 
+// Column blocks of a matrix: kBlockLanes lanes x vec columns each; a narrow
+// last block uses the smallest power-of-two lane count that covers it.
+// Tiles are kStreamWaves waves x rpw rows, rpw = base rows per wave, grown
+// for narrow blocks so that every tile has about the same number of
+// accesses.  Returns rpw.
+namespace {
+struct Block { int32_t col0, ncols, llog; };
+
+int matrix_blocks(int64_t n, int32_t vec, int base, std::vector<Block> &blocks)
+{
+    blocks.clear();
+    int blog = 0;
+    while ((1 << blog) < kBlockLanes) ++blog;
+    const int64_t lanes = n / vec;
+    const int64_t full = lanes >> blog, rem = lanes & ((int64_t(1) << blog) - 1);
+    for (int64_t b = 0; b < full; ++b)
+        blocks.push_back({static_cast<int32_t>((b << blog) * vec),
+                          static_cast<int32_t>((int64_t(1) << blog) * vec), blog});
+    if (rem > 0) {
+        int llog = 0;
+        while ((int64_t(1) << llog) < rem) ++llog;
+        blocks.push_back({static_cast<int32_t>((full << blog) * vec),
+                          static_cast<int32_t>(rem * vec), llog});
+    }
+    const int lead_llog = blocks.front().llog;
+    int rpw = base << (blog - (lead_llog < blog ? lead_llog : blog));
+    return rpw > kMaxRowsPerWave ? kMaxRowsPerWave : rpw;
+}
+}  // namespace
+
 rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::string &err)
 {
     if (count < 0 || (count > 0 && !t)) {
@@ -146,6 +176,25 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
             err = "tensor " + std::to_string(i) + ": factor pointer not 4-byte aligned";
             return RIKFAD_EALIGN;
         }
+    }
+
+    // A set with fewer matrix tiles than the chip has compute units leaves
+    // most of it idle, and its step lasts as long as one tile's chain of
+    // dependent row loads: halving the rows per wave doubles the tiles and
+    // shortens that chain.  Sets that fill the chip keep the full rows per
+    // wave, which streams at a higher rate.
+    int rpw_base = kRowsPerWave;
+    {
+        int64_t ntiles = 0;
+        std::vector<Block> blocks;
+        for (int64_t i = 0; i < count; ++i) {
+            const rikfad_tensor &T = t[i];
+            if (T.m == 1 || T.n == 1) continue;
+            const int rpw = matrix_blocks(T.n, matrix_vec(T), kRowsPerWave, blocks);
+            ntiles += static_cast<int64_t>(blocks.size()) *
+                      ceil_div(T.m, int64_t(kStreamWaves) * rpw);
+        }
+        if (ntiles < kSmallSetTiles && kRowsPerWave > 1) rpw_base = kRowsPerWave / 2;
     }
 
     int64_t ws = 0;
@@ -195,28 +244,8 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         pl.min_bytes += mn * (3 * eb + 8) + 8 * (T.m + T.n);   // x g p in, x p out; R C
         pl.stream_min_bytes += mn * (3 * eb + 8) + 4 * (T.m + T.n); // R, C read only
 
-        // Column blocks of kBlockLanes lanes x vec columns; a narrow last
-        // block uses the smallest power-of-two lane count that covers it.
-        // Tiles are kStreamWaves waves x rpw rows: rpw grows for narrow
-        // blocks so that every tile has about the same number of accesses.
-        struct Block { int32_t col0, ncols, llog; };
         std::vector<Block> blocks;
-        int blog = 0;
-        while ((1 << blog) < kBlockLanes) ++blog;
-        const int64_t lanes = T.n / d.vec;
-        const int64_t full = lanes >> blog, rem = lanes & ((int64_t(1) << blog) - 1);
-        for (int64_t b = 0; b < full; ++b)
-            blocks.push_back({static_cast<int32_t>((b << blog) * d.vec),
-                              static_cast<int32_t>((int64_t(1) << blog) * d.vec), blog});
-        if (rem > 0) {
-            int llog = 0;
-            while ((int64_t(1) << llog) < rem) ++llog;
-            blocks.push_back({static_cast<int32_t>((full << blog) * d.vec),
-                              static_cast<int32_t>(rem * d.vec), llog});
-        }
-        const int lead_llog = blocks.front().llog;
-        int rpw = kRowsPerWave << (blog - (lead_llog < blog ? lead_llog : blog));
-        if (rpw > kMaxRowsPerWave) rpw = kMaxRowsPerWave;
+        const int rpw = matrix_blocks(T.n, d.vec, rpw_base, blocks);
         const int64_t stripe_rows = int64_t(kStreamWaves) * rpw;
         d.ncb = static_cast<int32_t>(blocks.size());
         d.nrs = static_cast<int32_t>(ceil_div(T.m, stripe_rows));

@@ -222,8 +222,43 @@ static void check_plan(const Plan &pl, int64_t count)
     }
 }
 
+// Rows per wave of every matrix tile of a one-tensor fp32 set m x n.
+static int single_rpw(int64_t m, int64_t n, int64_t *ntiles)
+{
+    const uintptr_t base = uintptr_t(1) << 40;
+    rikfad_tensor t{};
+    t.x = reinterpret_cast<void *>(base);
+    t.g = reinterpret_cast<const void *>(base + (uintptr_t(1) << 36));
+    t.p = reinterpret_cast<float *>(base + (uintptr_t(2) << 36));
+    t.r = reinterpret_cast<float *>(base + (uintptr_t(3) << 36));
+    t.c = reinterpret_cast<float *>(base + (uintptr_t(4) << 36));
+    t.m = m;
+    t.n = n;
+    t.dtype = RIKFAD_FP32;
+    Plan pl;
+    std::string err;
+    if (plan_rikfad(&t, 1, pl, err) != RIKFAD_OK || pl.tiles.empty()) return -1;
+    int rpw = pl.tiles[0].rpw;
+    for (const Tile &tl : pl.tiles) if (tl.rpw != rpw) return -2;
+    *ntiles = static_cast<int64_t>(pl.tiles.size());
+    return rpw;
+}
+
 int main(int argc, char **argv)
 {
+    // A set with fewer tiles than compute units at the full rows per wave
+    // takes half of it; a set that fills the chip keeps it.
+    int64_t nt = 0;
+    CHECK(single_rpw(256, 512, &nt) == kRowsPerWave / 2 && nt == 32,
+          "256x512 set: rpw %d, %lld tiles", single_rpw(256, 512, &nt), (long long)nt);
+    CHECK(single_rpw(768, 3072, &nt) == kRowsPerWave && nt == 288,
+          "768x3072 set: rpw %d, %lld tiles", single_rpw(768, 3072, &nt), (long long)nt);
+    CHECK(single_rpw(1024, 2048, &nt) == kRowsPerWave && nt == 256,
+          "1024x2048 set (256 tiles): rpw %d", single_rpw(1024, 2048, &nt));
+    CHECK(single_rpw(992, 2048, &nt) == kRowsPerWave / 2 && nt == 496,
+          "992x2048 set (248 tiles at full rpw): rpw %d, %lld tiles", single_rpw(992, 2048, &nt),
+          (long long)nt);
+
     const int trials = argc > 1 ? std::atoi(argv[1]) : 300;
     std::mt19937_64 rng(12345);
     const int64_t dims[] = {1, 2, 3, 4, 5, 7, 8, 12, 16, 27, 31, 33, 63, 64, 65, 100, 127, 128,
