@@ -97,6 +97,19 @@ def test_multi_segment_finalisation(name, specs):
     assert_ok(errs, label=name)
 
 
+@pytest.mark.parametrize("m,tiles", [(992, 496), (1024, 256)])
+def test_small_set_rows_per_wave_threshold(m, tiles):
+    """m x 2048 fp32 just below (992 rows: 248 tiles at 4 rows per wave,
+    so the planner takes 2 rows per wave and 496 tiles) and at (1024 rows:
+    256 tiles, 4 rows per wave) the fewer-tiles-than-compute-units rule,
+    against the oracle in the friction-active setting, 12 steps."""
+    log(f"[case] rows-per-wave threshold {m}x2048")
+    pair, errs = run_parity([S("a", m, 2048)], synth.HP_FRICTION, 12, seed=6,
+                            label=f"threshold {m}x2048")
+    assert pair.opt.query()["stream_tiles"] == tiles
+    assert_ok(errs, label=f"threshold {m}")
+
+
 def test_misaligned_views_take_scalar_path():
     """Parameters and gradients that start one element into their buffers
     (not 16-byte aligned) still match the oracle."""
