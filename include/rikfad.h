@@ -63,8 +63,10 @@ typedef enum { RIKFAD_FP32 = 0, RIKFAD_BF16 = 1 } rikfad_dtype;
  * create to destroy, zero-fills p, r and c before the first step (the paper
  * starts from R = C = 0) unless it resumes a saved state, and never lets two
  * tensors of one context share memory.  Every pointer must be aligned to its
- * element size; 16-byte alignment (and n a multiple of 4 for fp32, of 8 for
- * bf16) selects the 128-bit load path, anything else a scalar path. */
+ * element size.  A matrix with n a multiple of 4 and x, g, p 16-byte aligned
+ * (fp32), or x, g 8-byte and p 16-byte aligned (bf16), takes the 4-wide
+ * path (128-bit accesses, 64-bit for bf16 x and g); any other matrix a
+ * one-column path in the same launch. */
 typedef struct {
     void *x;
     const void *g;
@@ -93,10 +95,14 @@ typedef struct rikfad_ctx rikfad_ctx;
 
 /* Create a context over `count` tensors (count >= 0; 0 gives a context whose
  * step does nothing).  Validates every argument before any HIP call, builds
- * the device tile tables and allocates the reduction workspace (about
- * 8 (m + n) bytes per matrix plus 4 m n/256 bytes of partial sums) on the
- * current HIP device.  The tensor array is copied; the buffers it points to
- * are not.  Zero-size tensors (m < 1 or n < 1) are rejected with
+ * the device tile tables and allocates the partial-sum workspace on the
+ * current HIP device: 4 (m B + S n + ceil(m / 256)) bytes per matrix for its
+ * B column blocks (256 columns, or 64 on the one-column path) and S row
+ * stripes (32 rows; 16 in a set with fewer matrix tiles than the chip has
+ * compute units; taller for narrow matrices) -- about 0.14 m n bytes
+ * (rikfad_query reports the total).  The tensor array is copied; the
+ * buffers it points to are not.  Zero-size tensors (m < 1 or n < 1) are
+ * rejected with
  * RIKFAD_EINVAL.
  *
  * Deferred form (default).  The second friction half-kick and D of step n
