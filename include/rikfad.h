@@ -102,8 +102,7 @@ typedef struct rikfad_ctx rikfad_ctx;
  * compute units; taller for narrow matrices) -- about 0.14 m n bytes
  * (rikfad_query reports the total).  The tensor array is copied; the
  * buffers it points to are not.  Zero-size tensors (m < 1 or n < 1) are
- * rejected with
- * RIKFAD_EINVAL.
+ * rejected with RIKFAD_EINVAL.
  *
  * Deferred form (default).  The second friction half-kick and D of step n
  * use the same factor R_{n+1}, C_{n+1} as the first half-kick of step n+1,
