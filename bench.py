@@ -50,6 +50,30 @@ def measured_traffic(dtype):
     return None if entry is None else entry.get("bytes_per_launch")
 
 
+# The chip's clocks ramp over the first ~20 ms of sustained load (shader
+# clock 2.1 -> 2.38 GHz on MI355X; a GPT2-S step goes from ~516 us in its
+# first ten steps to a steady ~424 us after about fifty) and drop again
+# when it idles, so every side measurement first keeps the GPU busy for
+# WARM_MS; the headline run takes its --warmup steps (default 100, ~42 ms).
+WARM_MS = 60.0
+
+
+def warm_up(step, count, warm_ms=WARM_MS):
+    """`count` untimed calls of step(), then more until the GPU has been
+    busy for at least warm_ms (synchronising every 8 calls)."""
+    import torch
+    for _ in range(count):
+        step()
+    if warm_ms <= 0:
+        return
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < warm_ms:
+        for _ in range(8):
+            step()
+        torch.cuda.synchronize()
+
+
 def build_workload(specs, dtype, seed, device, scales="lognormal"):
     """dtype None: each tensor in its own spec's storage type.  scales:
     "lognormal" row and column scales LogNormal(0, 0.5); "student_t" row
@@ -75,15 +99,15 @@ def build_workload(specs, dtype, seed, device, scales="lognormal"):
     return xs, gs
 
 
-def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0, scales="lognormal"):
+def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0, scales="lognormal",
+                warm_ms=WARM_MS):
     import torch
     from paper_2609_30342_amd import rikfad as R
     dev = torch.device("cuda:0")
     xs, gs = build_workload(specs, dtype, seed, dev, scales)
     opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
     info = opt.query()
-    for _ in range(warmup):
-        opt.step()
+    warm_up(opt.step, warmup, warm_ms)
     # Timed region: exactly `steps` steps, no per-kernel events.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -113,8 +137,7 @@ def time_ikfad(specs, hp, steps, warmup, seed=0, dtype="fp32"):
     from paper_2609_30342_amd import rikfad as R
     xs, gs = build_workload(specs, dtype, seed, torch.device("cuda:0"))
     ik = R.IKFAD(xs, gs, h=hp["h"], gamma=hp["gamma"], alpha=hp["alpha"], mu=hp["mu"])
-    for _ in range(warmup):
-        ik.step()
+    warm_up(ik.step, warmup)
     torch.cuda.synchronize()
     R.ikfad_timing_enable(ik.ctx, True)
     for _ in range(steps):
@@ -134,8 +157,7 @@ def time_adafm(specs, dtype, steps, warmup, seed=0, **hp):
     xs, gs = build_workload(specs, dtype, seed, torch.device("cuda:0"))
     opt = R.ADAFM(xs, gs, **hp)
     total, upd_bytes, state = R.adafm_min_bytes(opt.ctx)
-    for _ in range(warmup):
-        opt.step()
+    warm_up(opt.step, warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -166,8 +188,7 @@ def time_small(specs, hp, steps, warmup, seed=0):
     from paper_2609_30342_amd import rikfad as R
     xs, gs = build_workload(specs, None, seed, torch.device("cuda:0"))
     opt = R.RIKFAD(xs, gs, **hp)
-    for _ in range(warmup):
-        opt.step()
+    warm_up(opt.step, warmup)
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     a.record()
@@ -179,8 +200,7 @@ def time_small(specs, hp, steps, warmup, seed=0):
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         opt.step()
-    g.replay()
-    torch.cuda.synchronize()
+    warm_up(g.replay, 1)
     a.record()
     for _ in range(steps):
         g.replay()
@@ -205,7 +225,7 @@ def time_friction_report(m, n, iters=30, reps=3):
     gen = torch.Generator(device="cuda:0").manual_seed(7)
     xi = torch.rand((m, n), generator=gen, device="cuda:0")
     s = torch.cuda.current_stream().cuda_stream
-    R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s)
+    warm_up(lambda: R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s), 1)
     t0 = time.perf_counter()
     for _ in range(reps):
         R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s)
@@ -217,7 +237,7 @@ def time_friction_report(m, n, iters=30, reps=3):
             "gbps": passes * 4.0 * m * n / (ms * 1e-3) / 1e9}
 
 
-def time_probe(nfloat, reps=10):
+def time_probe(nfloat, reps=50):
     """3-read / 2-write fp32 stream of the same byte count as the step."""
     import torch
     from paper_2609_30342_amd import rikfad as R
@@ -226,7 +246,7 @@ def time_probe(nfloat, reps=10):
         b.normal_()
     s = torch.cuda.current_stream().cuda_stream
     ptrs = [b.data_ptr() for b in bufs]
-    R.rikfad_probe_stream(*ptrs, nfloat, s)
+    warm_up(lambda: R.rikfad_probe_stream(*ptrs, nfloat, s), 1)
     torch.cuda.synchronize()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
@@ -286,7 +306,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps before the timed ones (the clocks ramp over ~20 ms)")
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for cpu_baseline (0 = skip)")
@@ -310,7 +331,7 @@ def main():
     hp = dict(synth.HP_BASE)
     specs = synth.gpt2_small(args.dtype)
     N = sum(s.numel for s in specs)
-    main_run = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup)
+    main_run = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup, warm_ms=0.0)
     info = main_run["info"]
     stream_bytes = info["stream_min_bytes"]
     achieved = stream_bytes / (main_run["stream_ms"] * 1e-3) / 1e9
