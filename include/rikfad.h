@@ -181,11 +181,15 @@ rikfad_status rikfad_state_bytes(const rikfad_tensor *tensors, int64_t count,
  * Non-finite values are propagated, never masked. */
 rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out);
 
-/* Kernel timing with HIP events recorded on the step's stream around each
- * kernel of every subsequent step (enable != 0), for benchmarks.
- * rikfad_timing_read waits for the last recorded event and returns the
- * summed milliseconds of the streaming, finalisation and two-pass kernels
- * and the number of timed steps, then clears the record. */
+/* Kernel timing for benchmarks.  While enabled (enable != 0), every step
+ * attaches HIP start / stop events to the first and last kernel dispatch of
+ * each phase (hipExtLaunchKernelGGL), so they hold the kernels' own begin
+ * and end times and add nothing to the stream: a timed step runs like an
+ * untimed one.  Disabling and enabling again keeps the unread record.
+ * rikfad_timing_read waits for the last timed kernel and returns the
+ * summed milliseconds of the streaming, finalisation and two-pass apply
+ * kernels and the number of timed steps, then clears the record.  Each
+ * timed step holds 6 events until destroy. */
 rikfad_status rikfad_timing_enable(rikfad_ctx *ctx, int32_t enable);
 rikfad_status rikfad_timing_read(rikfad_ctx *ctx, double *stream_ms,
                                  double *finalize_ms, double *apply_ms,
@@ -221,6 +225,8 @@ rikfad_status ikfad_create(const ikfad_tensor *tensors, int64_t count,
                            const rikfad_hparams *hp, ikfad_ctx **out);
 rikfad_status ikfad_step(ikfad_ctx *ctx, void *stream);
 rikfad_status ikfad_set_hparams(ikfad_ctx *ctx, const rikfad_hparams *hp);
+/* Kernel timing as for rikfad_timing_*: ms = summed kernel time of the
+ * timed steps. */
 rikfad_status ikfad_timing_enable(ikfad_ctx *ctx, int32_t enable);
 rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps);
 void ikfad_destroy(ikfad_ctx *ctx);
@@ -318,8 +324,9 @@ rikfad_status adafm_min_bytes(const adafm_ctx *ctx, int64_t *min_bytes_per_step,
                               int64_t *update_min_bytes, int64_t *state_bytes);
 /* 1 if a non-finite R or C value was produced since create (blocks). */
 rikfad_status adafm_nonfinite(adafm_ctx *ctx, void *stream, int32_t *out);
-/* Per-step HIP event timing: ms4 = statistics pass, factor finalisation,
- * RMS pass + scale, update pass (sums over the steps since enable/read). */
+/* Kernel timing as for rikfad_timing_*: ms4 = statistics pass, factor
+ * finalisation, RMS pass + scale, update pass, summed over the timed
+ * steps since the last read. */
 rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable);
 rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms4, int64_t *steps);
 void adafm_destroy(adafm_ctx *ctx);

@@ -25,6 +25,7 @@
 
 #include "adafactor.hpp"
 #include "device.hpp"
+#include "launch.hpp"
 #include "layout.hpp"
 
 namespace rk {
@@ -452,17 +453,21 @@ struct PickUpdate {
 
 hipError_t launch_adafm_stats(const TensorDesc *tensors, const void *const *grads,
                               const Tile *tiles, const TileGroup *groups, int ngroups, float *ws,
-                              float *tilepart, const AdaCoeffs &k, bool x2, hipStream_t stream)
+                              float *tilepart, const AdaCoeffs &k, bool x2, hipStream_t stream,
+                              hipEvent_t start, hipEvent_t stop)
 {
+    const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const StatsFn fn = x2 ? pick<StatsFn>(gr, PickStats<true>())
                               : pick<StatsFn>(gr, PickStats<false>());
         if (!fn) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(gr.count)), dim3(kStreamThreads), 0,
-                           stream, tensors, grads, tiles, gr.begin, ws, tilepart, k);
-        const hipError_t e = hipGetLastError();
+        hipEvent_t a = start, b = q == last ? stop : nullptr;
+        start = nullptr;
+        const hipError_t e = launch(fn, dim3(static_cast<uint32_t>(gr.count)),
+                                    dim3(kStreamThreads), stream, a, b, tensors, grads, tiles,
+                                    gr.begin, ws, tilepart, k);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -470,43 +475,50 @@ hipError_t launch_adafm_stats(const TensorDesc *tensors, const void *const *grad
 
 hipError_t launch_adafm_rms(const TensorDesc *tensors, const void *const *grads,
                             const Tile *tiles, const TileGroup *groups, int ngroups,
-                            const float *ws, float *tilepart, hipStream_t stream)
+                            const float *ws, float *tilepart, hipStream_t stream,
+                            hipEvent_t start, hipEvent_t stop)
 {
+    const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const RmsFn fn = pick<RmsFn>(gr, PickRms());
         if (!fn) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(gr.count)), dim3(kStreamThreads), 0,
-                           stream, tensors, grads, tiles, gr.begin, ws, tilepart);
-        const hipError_t e = hipGetLastError();
+        hipEvent_t a = start, b = q == last ? stop : nullptr;
+        start = nullptr;
+        const hipError_t e = launch(fn, dim3(static_cast<uint32_t>(gr.count)),
+                                    dim3(kStreamThreads), stream, a, b, tensors, grads, tiles,
+                                    gr.begin, ws, tilepart);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
 hipError_t launch_adafm_scale(const TensorRange *ranges, int64_t ntensors, const float *tilepart,
-                              float *scales, const AdaCoeffs &k, hipStream_t stream)
+                              float *scales, const AdaCoeffs &k, hipStream_t stream,
+                              hipEvent_t start, hipEvent_t stop)
 {
     if (ntensors <= 0) return hipSuccess;
-    hipLaunchKernelGGL(adafm_scale_kernel, dim3(static_cast<uint32_t>(ntensors)), dim3(kThreads),
-                       0, stream, ranges, tilepart, scales, k);
-    return hipGetLastError();
+    return launch(adafm_scale_kernel, dim3(static_cast<uint32_t>(ntensors)), dim3(kThreads),
+                  stream, start, stop, ranges, tilepart, scales, k);
 }
 
 hipError_t launch_adafm_update(const TensorDesc *tensors, const void *const *grads,
                                const Tile *tiles, const TileGroup *groups, int ngroups,
                                const float *ws, const float *scales, const AdaCoeffs &k,
-                               hipStream_t stream)
+                               hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
+    const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const UpdateFn fn = pick<UpdateFn>(gr, PickUpdate());
         if (!fn) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(gr.count)), dim3(kStreamThreads), 0,
-                           stream, tensors, grads, tiles, gr.begin, ws, scales, k);
-        const hipError_t e = hipGetLastError();
+        hipEvent_t a = start, b = q == last ? stop : nullptr;
+        start = nullptr;
+        const hipError_t e = launch(fn, dim3(static_cast<uint32_t>(gr.count)),
+                                    dim3(kStreamThreads), stream, a, b, tensors, grads, tiles,
+                                    gr.begin, ws, scales, k);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

@@ -6,6 +6,7 @@
 // except the calls documented as blocking.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -129,30 +130,47 @@ struct GradRing {
     }
 };
 
-// Per-step event timing (benchmarks only): `per` events per step, one
-// before the first launch and one after each timed phase.
+// Per-step kernel timing (benchmarks only).  Each timed phase of a step has
+// a start and a stop event attached to its first and last kernel dispatch
+// (launch.hpp): they carry the kernels' own begin and end times and put no
+// packet of their own into the stream, so a timed step runs like an
+// untimed one.
 struct Timing {
-    explicit Timing(int per_step = 4) : per(per_step) {}
-    int per;
+    explicit Timing(int phases) : nph(phases) {}
+    int nph;
     bool on = false;
-    std::vector<hipEvent_t> ev;
+    std::vector<hipEvent_t> ev;     // 2 per phase and step
+    std::vector<uint8_t> ran;       // per phase and step: events attached
     int64_t steps = 0;
 
-    rikfad_status mark(int64_t step, int slot, hipStream_t stream)
+    // Events of phase ph of the step being enqueued (nullptr when off).
+    rikfad_status phase(int ph, hipEvent_t *start, hipEvent_t *stop)
     {
-        const size_t idx = static_cast<size_t>(step * per + slot);
-        while (ev.size() <= idx) {
+        *start = *stop = nullptr;
+        if (!on) return RIKFAD_OK;
+        const size_t slot = static_cast<size_t>(steps * nph + ph);
+        while (ev.size() < 2 * (slot + 1)) {
             hipEvent_t e;
             HIP_TRY(hipEventCreate(&e), "hipEventCreate timing");
             ev.push_back(e);
         }
-        HIP_TRY(hipEventRecord(ev[idx], stream), "hipEventRecord timing");
+        if (ran.size() < static_cast<size_t>((steps + 1) * nph))
+            ran.resize(static_cast<size_t>((steps + 1) * nph), 0);
+        ran[slot] = 1;
+        *start = ev[2 * slot];
+        *stop = ev[2 * slot + 1];
         return RIKFAD_OK;
+    }
+    void end_step()
+    {
+        if (on) steps += 1;
     }
     void release()
     {
         for (hipEvent_t e : ev) (void)hipEventDestroy(e);
         ev.clear();
+        ran.clear();
+        steps = 0;
     }
 };
 
@@ -162,7 +180,7 @@ struct rikfad_ctx {
     rk::Plan plan;
     DeviceTables dev;
     GradRing ring;
-    Timing timing;
+    Timing timing{3};          // streaming, finalisation, apply
     rikfad_hparams hp{};
     rk::Coeffs k{};
     bool two_pass = false;
@@ -175,7 +193,7 @@ struct adafm_ctx {
     rk::Plan plan;
     DeviceTables dev;
     GradRing ring;
-    Timing timing{5};
+    Timing timing{4};          // statistics, finalisation, RMS + scale, update
     adafm_hparams hp{};
     int64_t steps = 0;                      // steps taken
     std::vector<rk::TensorRange> ranges;    // tiles of each tensor
@@ -189,7 +207,7 @@ struct adafm_ctx {
 struct ikfad_ctx {
     rk::Plan plan;
     DeviceTables dev;
-    Timing timing;
+    Timing timing{1};
     rikfad_hparams hp{};
     rk::Coeffs k{};
 };
@@ -258,12 +276,13 @@ rikfad_status rikfad_create(const rikfad_tensor *tensors, int64_t count,
     return RIKFAD_OK;
 }
 
-static rikfad_status apply_pending(rikfad_ctx *ctx, hipStream_t stream)
+static rikfad_status apply_pending(rikfad_ctx *ctx, hipStream_t stream,
+                                   hipEvent_t start = nullptr, hipEvent_t stop = nullptr)
 {
     if (!ctx->pending) return RIKFAD_OK;
     hipError_t e = rk::launch_apply(ctx->dev.tensors, ctx->dev.tiles, ctx->plan.groups.data(),
                                     static_cast<int>(ctx->plan.groups.size()), ctx->dev.ws,
-                                    ctx->k, stream);
+                                    ctx->k, stream, start, stop);
     if (e != hipSuccess) return hip_fail(e, "launch apply kernel");
     ctx->pending = false;
     return RIKFAD_OK;
@@ -283,30 +302,32 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     }
     ctx->sums_valid = true;
     Timing &tm = ctx->timing;
+    hipEvent_t t0, t1;
     rikfad_status s;
-    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    if ((s = tm.phase(0, &t0, &t1)) != RIKFAD_OK) return s;
     e = rk::launch_stream(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles, pl.groups.data(),
                           static_cast<int>(pl.groups.size()), ctx->dev.ws, ctx->k,
-                          ctx->pending ? 1 : 0, stream);
+                          ctx->pending ? 1 : 0, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
     ctx->pending = false;
-    if (tm.on && (s = tm.mark(tm.steps, 1, stream)) != RIKFAD_OK) return s;
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
-    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin - pl.fold_items, ctx->dev.ws,
-                            ctx->k, ctx->dev.flag, 0, stream);
+    const int64_t nmain = nfin - pl.fold_items;
+    t0 = t1 = nullptr;
+    if (nmain > 0 && (s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
+    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nmain, ctx->dev.ws, ctx->k,
+                            ctx->dev.flag, 0, stream, t0, pl.fold_items > 0 ? nullptr : t1);
     if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
     if (pl.fold_items > 0) {
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + (nfin - pl.fold_items),
-                                pl.fold_items, ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream);
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + nmain, pl.fold_items,
+                                ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream, nullptr, t1);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
     }
-    if (tm.on && (s = tm.mark(tm.steps, 2, stream)) != RIKFAD_OK) return s;
     ctx->pending = pl.matrix_tiles > 0;
-    if (ctx->two_pass && (s = apply_pending(ctx, stream)) != RIKFAD_OK) return s;
-    if (tm.on) {
-        if ((s = tm.mark(tm.steps, 3, stream)) != RIKFAD_OK) return s;
-        tm.steps += 1;
+    if (ctx->two_pass && ctx->pending) {
+        if ((s = tm.phase(2, &t0, &t1)) != RIKFAD_OK) return s;
+        if ((s = apply_pending(ctx, stream, t0, t1)) != RIKFAD_OK) return s;
     }
+    tm.end_step();
     return RIKFAD_OK;
 }
 
@@ -397,26 +418,27 @@ rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out)
     return RIKFAD_OK;
 }
 
-// Sums over the timed steps of the per - 1 phase durations into ms[].
+// Sums over the timed steps of each phase's kernel time into ms[0..nph-1]
+// and clears the record.
 static rikfad_status read_timing(Timing &tm, double *ms, int64_t *steps)
 {
-    const int per = tm.per;
-    for (int k = 0; k + 1 < per; ++k) ms[k] = 0.0;
-    if (tm.steps > 0) {
-        HIP_TRY(hipEventSynchronize(tm.ev[static_cast<size_t>(tm.steps * per - 1)]),
-                "hipEventSynchronize timing");
-        for (int64_t s = 0; s < tm.steps; ++s) {
-            for (int k = 0; k + 1 < per; ++k) {
-                float t = 0.f;
-                HIP_TRY(hipEventElapsedTime(&t, tm.ev[static_cast<size_t>(s * per + k)],
-                                            tm.ev[static_cast<size_t>(s * per + k + 1)]),
-                        "hipEventElapsedTime");
-                ms[k] += t;
-            }
+    for (int k = 0; k < tm.nph; ++k) ms[k] = 0.0;
+    const size_t slots = static_cast<size_t>(tm.steps * tm.nph);
+    for (size_t q = slots; q-- > 0;) {          // wait for the last attached stop event
+        if (q < tm.ran.size() && tm.ran[q]) {
+            HIP_TRY(hipEventSynchronize(tm.ev[2 * q + 1]), "hipEventSynchronize timing");
+            break;
         }
+    }
+    for (size_t q = 0; q < slots && q < tm.ran.size(); ++q) {
+        if (!tm.ran[q]) continue;
+        float t = 0.f;
+        HIP_TRY(hipEventElapsedTime(&t, tm.ev[2 * q], tm.ev[2 * q + 1]), "hipEventElapsedTime");
+        ms[q % static_cast<size_t>(tm.nph)] += t;
     }
     *steps = tm.steps;
     tm.steps = 0;
+    std::fill(tm.ran.begin(), tm.ran.end(), 0);
     return RIKFAD_OK;
 }
 
@@ -424,7 +446,6 @@ rikfad_status rikfad_timing_enable(rikfad_ctx *ctx, int32_t enable)
 {
     if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
     ctx->timing.on = enable != 0;
-    ctx->timing.steps = 0;
     return RIKFAD_OK;
 }
 
@@ -486,16 +507,14 @@ rikfad_status ikfad_step(ikfad_ctx *ctx, void *stream_)
     hipStream_t stream = static_cast<hipStream_t>(stream_);
     if (ctx->plan.tiles.empty()) return RIKFAD_OK;
     Timing &tm = ctx->timing;
+    hipEvent_t t0, t1;
     rikfad_status s;
-    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    if ((s = tm.phase(0, &t0, &t1)) != RIKFAD_OK) return s;
     hipError_t e = rk::launch_ikfad(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
-                                    static_cast<int64_t>(ctx->plan.tiles.size()), ctx->k, stream);
+                                    static_cast<int64_t>(ctx->plan.tiles.size()), ctx->k, stream,
+                                    t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch ikfad kernel");
-    if (tm.on) {
-        for (int k = 1; k < 4; ++k)
-            if ((s = tm.mark(tm.steps, k, stream)) != RIKFAD_OK) return s;
-        tm.steps += 1;
-    }
+    tm.end_step();
     return RIKFAD_OK;
 }
 
@@ -514,14 +533,13 @@ rikfad_status ikfad_timing_enable(ikfad_ctx *ctx, int32_t enable)
 {
     if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
     ctx->timing.on = enable != 0;
-    ctx->timing.steps = 0;
     return RIKFAD_OK;
 }
 
 rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps)
 {
     if (!ctx || !ms || !steps) return fail(RIKFAD_EINVAL, "NULL argument");
-    double t[3];
+    double t[1];
     rikfad_status s = read_timing(ctx->timing, t, steps);
     if (s != RIKFAD_OK) return s;
     *ms = t[0];
@@ -681,41 +699,44 @@ rikfad_status adafm_step(adafm_ctx *ctx, void *stream_)
     fk.kappa = k.omb;
     const int ng = static_cast<int>(pl.groups.size());
     Timing &tm = ctx->timing;
+    hipEvent_t t0, t1;
     rikfad_status s;
-    if (tm.on && (s = tm.mark(tm.steps, 0, stream)) != RIKFAD_OK) return s;
+    if ((s = tm.phase(0, &t0, &t1)) != RIKFAD_OK) return s;
     hipError_t e = rk::launch_adafm_stats(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
                                           pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, k,
-                                          ctx->hp.scale_parameter != 0, stream);
+                                          ctx->hp.scale_parameter != 0, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch adafm stats kernel");
-    if (tm.on && (s = tm.mark(tm.steps, 1, stream)) != RIKFAD_OK) return s;
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
-    if (nfin > 0) {
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin - pl.fold_items, ctx->dev.ws,
-                                fk, ctx->dev.flag, 0, stream);
+    const int64_t nmain = nfin - pl.fold_items;
+    if (nmain > 0) {
+        if ((s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nmain, ctx->dev.ws, fk,
+                                ctx->dev.flag, 0, stream, t0, pl.fold_items > 0 ? nullptr : t1);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
         if (pl.fold_items > 0) {
-            e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + (nfin - pl.fold_items),
-                                    pl.fold_items, ctx->dev.ws, fk, ctx->dev.flag, 0, stream);
+            e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + nmain, pl.fold_items,
+                                    ctx->dev.ws, fk, ctx->dev.flag, 0, stream, nullptr, t1);
             if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
         }
     }
-    if (tm.on && (s = tm.mark(tm.steps, 2, stream)) != RIKFAD_OK) return s;
+    // RMS pass (when clipping and there are matrices) and the scale kernel:
+    // one timed phase from the first of them to the scale kernel.
+    if ((s = tm.phase(2, &t0, &t1)) != RIKFAD_OK) return s;
     if (ctx->hp.clip_threshold > 0 && pl.matrix_tiles > 0) {
         e = rk::launch_adafm_rms(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
-                                 pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, stream);
+                                 pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, stream, t0,
+                                 nullptr);
         if (e != hipSuccess) return hip_fail(e, "launch adafm rms kernel");
+        t0 = nullptr;
     }
     e = rk::launch_adafm_scale(ctx->ranges_dev, static_cast<int64_t>(pl.tensors.size()),
-                               ctx->tilepart, ctx->scales, k, stream);
+                               ctx->tilepart, ctx->scales, k, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch adafm scale kernel");
-    if (tm.on && (s = tm.mark(tm.steps, 3, stream)) != RIKFAD_OK) return s;
+    if ((s = tm.phase(3, &t0, &t1)) != RIKFAD_OK) return s;
     e = rk::launch_adafm_update(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles, pl.groups.data(),
-                                ng, ctx->dev.ws, ctx->scales, k, stream);
+                                ng, ctx->dev.ws, ctx->scales, k, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch adafm update kernel");
-    if (tm.on) {
-        if ((s = tm.mark(tm.steps, 4, stream)) != RIKFAD_OK) return s;
-        tm.steps += 1;
-    }
+    tm.end_step();
     ctx->steps = t;
     return RIKFAD_OK;
 }
@@ -791,7 +812,6 @@ rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable)
 {
     if (!ctx) return fail(RIKFAD_EINVAL, "ctx is NULL");
     ctx->timing.on = enable != 0;
-    ctx->timing.steps = 0;
     return RIKFAD_OK;
 }
 

@@ -24,6 +24,7 @@
 
 #include "device.hpp"
 #include "kernels.hpp"
+#include "launch.hpp"
 #include "layout.hpp"
 
 namespace rk {
@@ -455,24 +456,26 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(
 
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
                          const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
-                         int pending, hipStream_t stream)
+                         int pending, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
+    const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
-#define RK_LAUNCH(XT, V)                                                                     \
-    hipLaunchKernelGGL((rikfad_stream_kernel<XT, V>), grid, block, 0, stream, tensors, grads, \
-                       tiles, gr.begin, gr.count, ws, k, pending)
-        if (gr.dtype == DT_F32) {
-            if (gr.vec == 4) RK_LAUNCH(float, 4);
-            else RK_LAUNCH(float, 1);
-        } else {
-            if (gr.vec == 4) RK_LAUNCH(uint16_t, 4);
-            else RK_LAUNCH(uint16_t, 1);
-        }
-#undef RK_LAUNCH
-        hipError_t e = hipGetLastError();
+        hipEvent_t a = start, b = q == last ? stop : nullptr;
+        start = nullptr;
+        hipError_t e;
+        if (gr.dtype == DT_F32)
+            e = gr.vec == 4 ? launch(rikfad_stream_kernel<float, 4>, grid, block, stream, a, b,
+                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending)
+                            : launch(rikfad_stream_kernel<float, 1>, grid, block, stream, a, b,
+                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending);
+        else
+            e = gr.vec == 4 ? launch(rikfad_stream_kernel<uint16_t, 4>, grid, block, stream, a,
+                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending)
+                            : launch(rikfad_stream_kernel<uint16_t, 1>, grid, block, stream, a,
+                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -480,40 +483,41 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
 
 hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
                            float *ws, const Coeffs &k, int *flag, int init_only,
-                           hipStream_t stream)
+                           hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     if (nitems <= 0) return hipSuccess;
-    hipLaunchKernelGGL(rikfad_finalize_kernel, dim3(static_cast<uint32_t>(nitems)),
-                       dim3(kThreads), 0, stream, tensors, items, ws, k, flag, init_only);
-    return hipGetLastError();
+    return launch(rikfad_finalize_kernel, dim3(static_cast<uint32_t>(nitems)), dim3(kThreads),
+                  stream, start, stop, tensors, items, ws, k, flag, init_only);
 }
 
 hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,
-                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream)
+                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream,
+                        hipEvent_t start, hipEvent_t stop)
 {
+    const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
         const dim3 grid(static_cast<uint32_t>(gr.count)), block(kStreamThreads);
-        if (gr.vec == 4)
-            hipLaunchKernelGGL(rikfad_apply_kernel<4>, grid, block, 0, stream, tensors, tiles,
-                               gr.begin, ws, k);
-        else
-            hipLaunchKernelGGL(rikfad_apply_kernel<1>, grid, block, 0, stream, tensors, tiles,
-                               gr.begin, ws, k);
-        hipError_t e = hipGetLastError();
+        hipEvent_t a = start, b = q == last ? stop : nullptr;
+        start = nullptr;
+        const hipError_t e =
+            gr.vec == 4 ? launch(rikfad_apply_kernel<4>, grid, block, stream, a, b, tensors,
+                                 tiles, gr.begin, ws, k)
+                        : launch(rikfad_apply_kernel<1>, grid, block, stream, a, b, tensors,
+                                 tiles, gr.begin, ws, k);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                        int64_t ntiles, const Coeffs &k, hipStream_t stream)
+                        int64_t ntiles, const Coeffs &k, hipStream_t stream, hipEvent_t start,
+                        hipEvent_t stop)
 {
     if (ntiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(ikfad_kernel, dim3(static_cast<uint32_t>(ntiles)), dim3(kThreads), 0,
-                       stream, tensors, grads, tiles, k);
-    return hipGetLastError();
+    return launch(ikfad_kernel, dim3(static_cast<uint32_t>(ntiles)), dim3(kThreads), stream,
+                  start, stop, tensors, grads, tiles, k);
 }
 
 static uint32_t probe_grid(int64_t units)

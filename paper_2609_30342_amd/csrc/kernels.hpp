@@ -7,24 +7,31 @@
 
 namespace rk {
 
+// Each launcher takes optional timing events: `start` is attached to its
+// first dispatch and `stop` to its last (see launch.hpp).
+
 // Streaming pass over all tiles (matrix and vector) of a context: one
 // launch per tile group.
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
                          const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
-                         int pending, hipStream_t stream);
+                         int pending, hipStream_t stream, hipEvent_t start = nullptr,
+                         hipEvent_t stop = nullptr);
 
 // Finalisation of R, C and the partial sums of R (init_only: sums only).
 hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
                            float *ws, const Coeffs &k, int *flag, int init_only,
-                           hipStream_t stream);
+                           hipStream_t stream, hipEvent_t start = nullptr,
+                           hipEvent_t stop = nullptr);
 
 // Second half-kick + D over the matrix tiles of every tile group.
 hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,
-                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream);
+                        int ngroups, const float *ws, const Coeffs &k, hipStream_t stream,
+                        hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 // Full-tensor element-wise iKFAD.
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                        int64_t ntiles, const Coeffs &k, hipStream_t stream);
+                        int64_t ntiles, const Coeffs &k, hipStream_t stream,
+                        hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 hipError_t launch_probe_stream(const float *a, const float *b, const float *c, float *d,
                                float *e, int64_t nfloat, hipStream_t stream);
