@@ -410,6 +410,7 @@ def main():
             "stream_ms": rb["stream_ms"],
             "stream_gbps": rb["info"]["stream_min_bytes"] / (rb["stream_ms"] * 1e-3) / 1e9}
         var["probe_3r2w_gbps"] = time_probe(N)
+        var["stream_kernel_vs_probe"] = achieved / var["probe_3r2w_gbps"]
         var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {
             "single_256x512_fp32": time_small(synth.single_matrix(), hp, 200, 5),
