@@ -160,6 +160,20 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
 // Each entry carries its own friction xi: half-kick with xi_n, exact
 // friction update driven by P^(1), half-kick with xi_{n+1}, then D.
 
+template <int V>
+__device__ __forceinline__ void ikfad_math(float (&xv)[V], const float (&gv)[V], float (&pv)[V],
+                                           float (&fv)[V], const Coeffs &k)
+{
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+        const float pb = kick(pv[i], gv[i], k);
+        xv[i] = xv[i] + k.h * pb;
+        const float p1 = pb * exp2f(k.kh * fv[i]);
+        fv[i] = k.a * fv[i] + k.kappa * (p1 * p1);
+        pv[i] = damp(p1 * exp2f(k.kh * fv[i]), k);
+    }
+}
+
 template <typename XT, int V>
 __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__restrict__ g,
                                             float *__restrict__ p, float *__restrict__ xi,
@@ -170,26 +184,45 @@ __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__rest
     Io<XT, V>::load(g, gv);
     Io<float, V>::load(p, pv);
     Io<float, V>::load(xi, fv);
-#pragma unroll
-    for (int i = 0; i < V; ++i) {
-        const float pb = kick(pv[i], gv[i], k);
-        xv[i] = xv[i] + k.h * pb;
-        const float p1 = pb * exp2f(k.kh * fv[i]);
-        fv[i] = k.a * fv[i] + k.kappa * (p1 * p1);
-        pv[i] = damp(p1 * exp2f(k.kh * fv[i]), k);
-    }
+    ikfad_math<V>(xv, gv, pv, fv, k);
     Io<XT, V>::store(x, xv);
     Io<float, V>::store(p, pv);
     Io<float, V>::store(xi, fv);
 }
 
-template <typename XT, int V, int NTH>
+// Elements start .. start + count - 1, V per thread access.  With U > 1,
+// batches of U accesses per thread send every load of the batch before its
+// first store (more bytes in flight; costs registers, so only the
+// full-tensor iKFAD kernel's fp32 path uses it).
+template <typename XT, int V, int NTH, int U = 1>
 __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
                                   float *__restrict__ p, float *__restrict__ xi,
                                   int64_t start, int count, const Coeffs &k)
 {
     const int full = count - count % V;
-    for (int e = threadIdx.x * V; e < full; e += NTH * V) {
+    int e = threadIdx.x * V;
+    if (U > 1) {
+        for (; e + (U - 1) * NTH * V < full; e += U * NTH * V) {
+            float xv[U][V], gv[U][V], pv[U][V], fv[U][V];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t o = start + e + u * NTH * V;
+                Io<XT, V>::load(x + o, xv[u]);
+                Io<XT, V>::load(g + o, gv[u]);
+                Io<float, V>::load(p + o, pv[u]);
+                Io<float, V>::load(xi + o, fv[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t o = start + e + u * NTH * V;
+                ikfad_math<V>(xv[u], gv[u], pv[u], fv[u], k);
+                Io<XT, V>::store(x + o, xv[u]);
+                Io<float, V>::store(p + o, pv[u]);
+                Io<float, V>::store(xi + o, fv[u]);
+            }
+        }
+    }
+    for (; e < full; e += NTH * V) {
         const int64_t o = start + e;
         ikfad_elems<XT, V>(x + o, g + o, p + o, xi + o, k);
     }
@@ -199,7 +232,7 @@ __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
     }
 }
 
-template <typename XT, int NTH>
+template <typename XT, int NTH, int U4 = 1>
 __device__ void elementwise_tile(const TensorDesc &td, const void *g, const Tile &tile,
                                  const Coeffs &k)
 {
@@ -208,7 +241,7 @@ __device__ void elementwise_tile(const TensorDesc &td, const void *g, const Tile
     if (tile.vec == 8)
         elementwise_range<XT, 8, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
     else if (tile.vec == 4)
-        elementwise_range<XT, 4, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 4, NTH, U4>(x, gg, td.p, td.xi, tile.start, tile.count, k);
     else
         elementwise_range<XT, 1, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
 }
@@ -400,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void ikfad_kernel(
     const Tile tile = tiles[blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
-    if (tile.dtype == DT_F32) elementwise_tile<float, kThreads>(td, g, tile, k);
+    if (tile.dtype == DT_F32) elementwise_tile<float, kThreads, kVecIters>(td, g, tile, k);
     else elementwise_tile<uint16_t, kThreads>(td, g, tile, k);
 }
 
