@@ -296,8 +296,8 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     if (pl.tiles.empty()) return RIKFAD_OK;
     hipError_t e;
     if (!ctx->sums_valid && pl.row_items > 0) {
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, pl.row_items, ctx->dev.ws, ctx->k,
-                                ctx->dev.flag, 1, stream);
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, pl.row_items, pl.fin_log2,
+                                ctx->dev.ws, ctx->k, ctx->dev.flag, 1, stream);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (init)");
     }
     ctx->sums_valid = true;
@@ -311,17 +311,11 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
     ctx->pending = false;
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
-    const int64_t nmain = nfin - pl.fold_items;
     t0 = t1 = nullptr;
-    if (nmain > 0 && (s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
-    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nmain, ctx->dev.ws, ctx->k,
-                            ctx->dev.flag, 0, stream, t0, pl.fold_items > 0 ? nullptr : t1);
+    if (nfin > 0 && (s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
+    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
+                            ctx->k, ctx->dev.flag, 0, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
-    if (pl.fold_items > 0) {
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + nmain, pl.fold_items,
-                                ctx->dev.ws, ctx->k, ctx->dev.flag, 0, stream, nullptr, t1);
-        if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
-    }
     ctx->pending = pl.matrix_tiles > 0;
     if (ctx->two_pass && ctx->pending) {
         if ((s = tm.phase(2, &t0, &t1)) != RIKFAD_OK) return s;
@@ -707,17 +701,11 @@ rikfad_status adafm_step(adafm_ctx *ctx, void *stream_)
                                           ctx->hp.scale_parameter != 0, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch adafm stats kernel");
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
-    const int64_t nmain = nfin - pl.fold_items;
-    if (nmain > 0) {
+    if (nfin > 0) {
         if ((s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nmain, ctx->dev.ws, fk,
-                                ctx->dev.flag, 0, stream, t0, pl.fold_items > 0 ? nullptr : t1);
+        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
+                                fk, ctx->dev.flag, 0, stream, t0, t1);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
-        if (pl.fold_items > 0) {
-            e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin + nmain, pl.fold_items,
-                                    ctx->dev.ws, fk, ctx->dev.flag, 0, stream, nullptr, t1);
-            if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (fold)");
-        }
     }
     // RMS pass (when clipping and there are matrices) and the scale kernel:
     // one timed phase from the first of them to the scale kernel.

@@ -273,17 +273,24 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
         stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
 }
 
-// Finalisation (C.2 / C.3 stage 2).  Row items: thread t owns row start+t,
-// sums its column-block partials in block order, updates R, and the
-// workgroup writes the fixed-order sum of its 256 new R values.  Column
-// items sum one segment of row stripes for 64 columns; tall tensors have
-// several segments, folded in segment order by a second, small launch.
-// init_only recomputes the partial sums of R from R as it stands.
-__global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
+// Finalisation (C.2 / C.3 stage 2), one launch.  Row items: thread t owns
+// row start+t, sums its column-block partials in block order, updates R,
+// and the workgroup writes the fixed-order sum of each 256 new R values.
+// Column items: thread (q, c) of S stripe lanes x W = 256 / S columns sums
+// the stripes q, q + S, q + 2S, ... of column start+c in that order
+// (kColLoads loads in flight), and the S lane sums of a column are folded
+// pairwise through LDS (lane q takes lane q + h for h = S/2, ..., 1): a
+// fixed tree, so the result does not depend on timing.  init_only
+// recomputes the partial sums of R from R as it stands.
+template <int LOG2T>
+__global__ __launch_bounds__(1 << LOG2T) void rikfad_finalize_kernel(
     const TensorDesc *__restrict__ tensors, const FinItem *__restrict__ items,
     float *__restrict__ ws, Coeffs k, int *__restrict__ flag, int init_only)
 {
-    __shared__ float lds[kThreads];
+    constexpr int T = 1 << LOG2T;
+    static_assert(T % kChunkRows == 0 && kChunkRows == 4 * kWave,
+                  "row items cover whole 256-row chunks, four waves each");
+    __shared__ float lds[T];
     const FinItem it = items[blockIdx.x];
     const TensorDesc td = tensors[it.tensor];
     if (it.kind == FIN_ROWS) {
@@ -295,78 +302,64 @@ __global__ __launch_bounds__(kThreads) void rikfad_finalize_kernel(
             if (!init_only) {
                 const RK_GLOBAL float *rp = gmem(ws) + td.rowpart + i;
                 float s = 0.f;
-                for (int cb = 0; cb < td.ncb; cb += 8) {
-                    float v[8];
+                for (int cb = 0; cb < td.ncb; cb += 16) {
+                    float v[16];
 #pragma unroll
-                    for (int q = 0; q < 8; ++q)
+                    for (int q = 0; q < 16; ++q)
                         v[q] = cb + q < td.ncb ? rp[static_cast<int64_t>(cb + q) * td.m] : 0.f;
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) s += v[q];
+                    for (int q = 0; q < 16; ++q) s += v[q];
                 }
                 rv = k.a * rv + k.kappa * s;
                 gmem(td.r)[i] = rv;
             }
             if (!isfinite(rv)) *gmem(flag) = 1;
         }
+        // One partial sum of R per 256 rows (four waves, folded in order).
         float v = rv;
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o);
         if ((threadIdx.x & (kWave - 1)) == 0) lds[threadIdx.x >> 6] = v;
         __syncthreads();
-        if (threadIdx.x == 0) {
-            const float s = ((lds[0] + lds[1]) + lds[2]) + lds[3];
-            gmem(ws)[td.chunk + it.chunk] = s;
+        const int q = threadIdx.x;
+        if (q < T / kChunkRows && q * kChunkRows < it.count) {
+            const float *l = lds + 4 * q;
+            const float s = ((l[0] + l[1]) + l[2]) + l[3];
+            gmem(ws)[td.chunk + it.chunk + q] = s;
             if (!isfinite(s)) *gmem(flag) = 1;
         }
-    } else if (it.kind == FIN_COLS) {
-        // Wave q sums stripes [seg0 + 16 q, seg0 + 16 q + 16) of the 64
-        // columns (each load a coalesced 256-byte row), in stripe order;
-        // the four waves are folded in wave order.
-        const int j = threadIdx.x & (kWave - 1);
-        const int q = threadIdx.x >> 6;
-        const int seg0 = it.chunk * kSegStripes;
-        const int s0 = min(td.nrs, seg0 + q * (kSegStripes / 4));
-        const int s1 = min(td.nrs, s0 + kSegStripes / 4);
-        float s = 0.f;
-        if (j < it.count) {
-            const RK_GLOBAL float *cp = gmem(ws) + td.colpart + it.start + j;
-            float v[kSegStripes / 4];
-#pragma unroll
-            for (int u = 0; u < kSegStripes / 4; ++u)
-                v[u] = s0 + u < s1 ? cp[static_cast<int64_t>(s0 + u) * td.n] : 0.f;
-#pragma unroll
-            for (int u = 0; u < kSegStripes / 4; ++u) s += v[u];
-        }
-        lds[threadIdx.x] = s;
-        __syncthreads();
-        if (q == 0 && j < it.count) {
-            const float cs = ((lds[j] + lds[kWave + j]) + lds[2 * kWave + j]) + lds[3 * kWave + j];
-            const int64_t jj = static_cast<int64_t>(it.start) + j;
-            if (td.nseg > 1) {
-                gmem(ws)[td.colseg + static_cast<int64_t>(it.chunk) * td.n + jj] = cs;
-            } else {
-                const float cvn = k.a * gmem(td.c)[jj] + k.kappa * cs;
-                gmem(td.c)[jj] = cvn;
-                if (!isfinite(cvn)) *gmem(flag) = 1;
-            }
-        }
     } else {
-        // FIN_FOLD: thread t owns column start + t and adds its segment sums
-        // in segment order.
-        const int t = threadIdx.x;
-        if (t < it.count) {
-            const int64_t jj = static_cast<int64_t>(it.start) + t;
-            const RK_GLOBAL float *sp = gmem(ws) + td.colseg + jj;
-            float cs = 0.f;
-            for (int q0 = 0; q0 < td.nseg; q0 += 16) {
-                float v[16];
+        const int slog = it.lanes_log2;
+        const int S = 1 << slog;
+        const int W = T >> slog;
+        const int c = threadIdx.x & (W - 1);
+        const int q = threadIdx.x >> (LOG2T - slog);
+        float s = 0.f;
+        if (c < it.count) {
+            const RK_GLOBAL float *cp = gmem(ws) + td.colpart + it.start + c;
+            for (int s0 = q; s0 < td.nrs; s0 += S * kColLoads) {
+                float v[kColLoads];
 #pragma unroll
-                for (int u = 0; u < 16; ++u)
-                    v[u] = q0 + u < td.nseg ? sp[static_cast<int64_t>(q0 + u) * td.n] : 0.f;
+                for (int u = 0; u < kColLoads; ++u) {
+                    const int st = s0 + u * S;
+                    v[u] = st < td.nrs ? cp[static_cast<int64_t>(st) * td.n] : 0.f;
+                }
 #pragma unroll
-                for (int u = 0; u < 16; ++u) cs += v[u];
+                for (int u = 0; u < kColLoads; ++u) s += v[u];
             }
-            const float cvn = k.a * gmem(td.c)[jj] + k.kappa * cs;
+        }
+        if (slog > 0) {
+            lds[threadIdx.x] = s;
+            for (int h = S >> 1; h > 0; h >>= 1) {
+                __syncthreads();
+                if (q < h) lds[threadIdx.x] += lds[threadIdx.x + h * W];
+            }
+            __syncthreads();
+            s = lds[c];
+        }
+        if (q == 0 && c < it.count) {
+            const int64_t jj = static_cast<int64_t>(it.start) + c;
+            const float cvn = k.a * gmem(td.c)[jj] + k.kappa * s;
             gmem(td.c)[jj] = cvn;
             if (!isfinite(cvn)) *gmem(flag) = 1;
         }
@@ -515,12 +508,16 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
 }
 
 hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
-                           float *ws, const Coeffs &k, int *flag, int init_only,
+                           int fin_log2, float *ws, const Coeffs &k, int *flag, int init_only,
                            hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     if (nitems <= 0) return hipSuccess;
-    return launch(rikfad_finalize_kernel, dim3(static_cast<uint32_t>(nitems)), dim3(kThreads),
-                  stream, start, stop, tensors, items, ws, k, flag, init_only);
+    const dim3 grid(static_cast<uint32_t>(nitems));
+    if (fin_log2 == kFinLargeLog2)
+        return launch(rikfad_finalize_kernel<kFinLargeLog2>, grid, dim3(1 << kFinLargeLog2),
+                      stream, start, stop, tensors, items, ws, k, flag, init_only);
+    return launch(rikfad_finalize_kernel<kFinSmallLog2>, grid, dim3(1 << kFinSmallLog2), stream,
+                  start, stop, tensors, items, ws, k, flag, init_only);
 }
 
 hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,

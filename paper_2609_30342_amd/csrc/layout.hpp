@@ -13,6 +13,7 @@ namespace rk {
 #endif
 constexpr int kWave = 64;                       // CDNA wavefront
 constexpr int kThreads = 256;                   // workgroup of the small kernels
+constexpr int kThreadsLog2 = 8;
 constexpr int kStreamWaves = RK_STREAM_WAVES;   // waves per streaming workgroup
 constexpr int kStreamThreads = kWave * kStreamWaves;
 #ifndef RK_RING_F32
@@ -38,10 +39,15 @@ constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kV
 
 enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 enum : int32_t { KIND_MATRIX = 0, KIND_VECTOR = 1 };
-enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1, FIN_FOLD = 2 };
+enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1 };
 
-constexpr int kSegStripes = 64;                 // stripes per column-sum segment
-constexpr int kFoldCols = 256;                  // columns per fold item
+// Finalisation workgroups: 256 threads, or 1024 for sets with a matrix of
+// more than 512 row stripes (about 16K rows), whose column items need more
+// stripe lanes than 256 threads hold at 16 columns each.
+constexpr int kFinSmallLog2 = 8;
+constexpr int kFinLargeLog2 = 10;
+constexpr int kColLoads = 32;                   // column partials in flight per thread
+constexpr int kMinColsLog2 = 4;                 // at least 16 columns (64 bytes) per column item
 
 // One parameter tensor.  Offsets are in floats into the context workspace.
 struct TensorDesc {
@@ -54,9 +60,8 @@ struct TensorDesc {
     int64_t rowpart;   // [ncb][m] row partial sums of [P^(1)]^2
     int64_t colpart;   // [nrs][n] column partial sums of [P^(1)]^2
     int64_t chunk;     // [nchunk] partial sums of R
-    int64_t colseg;    // [nseg][n] segment sums of the column partials (nseg > 1)
     int32_t nchunk, ncb, nrs, dtype;
-    int32_t kind, vec, nseg, pad1;
+    int32_t kind, vec;
 };
 
 // One workgroup of the streaming pass.
@@ -88,19 +93,20 @@ struct TileGroup {
     int64_t count;
 };
 
-// One workgroup of the finalisation passes.
-//   FIN_ROWS  256 rows: R update and one partial sum of R.
-//   FIN_COLS  64 columns x one segment of up to kSegStripes stripes: a
-//             segment sum, or the C update when the tensor has one segment.
-//   FIN_FOLD  256 columns of a tensor with several segments: C update from
-//             the segment sums (second launch).
+// One workgroup of the finalisation pass (one launch).
+//   FIN_ROWS  T rows (T = threads of the workgroup): R update and one
+//             partial sum of R per 256 rows.
+//   FIN_COLS  T / S columns, all row stripes: C update.  The T threads are
+//             S = 2^lanes_log2 stripe lanes x T / S columns, S the smallest
+//             power of two that leaves each thread at most kColLoads
+//             stripes, capped so that an item keeps at least 16 columns.
 struct FinItem {
     int32_t tensor;
     int32_t kind;
     int32_t start;     // first row / column
     int32_t count;     // rows / columns
-    int32_t chunk;     // FIN_ROWS: partial sum of R written; FIN_COLS: segment
-    int32_t pad;
+    int32_t chunk;     // FIN_ROWS: the partial sum of R it writes
+    int32_t lanes_log2;// FIN_COLS: log2 of the stripe lanes S
 };
 
 // Step coefficients, computed in fp64 on the host and rounded once.

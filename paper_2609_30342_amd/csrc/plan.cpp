@@ -206,7 +206,7 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     const int32_t class_vec[4] = {4, 1, 4, 1};
     std::vector<Tile> mat_tiles[4];
     std::vector<Tile> vec_tiles[2];
-    std::vector<FinItem> col_items, fold_items;
+    std::vector<FinItem> col_items;
     for (int64_t i = 0; i < count; ++i) {
         const rikfad_tensor &T = t[i];
         TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
@@ -278,29 +278,28 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                 mat_tiles[cls].push_back(tl);
             }
         }
-        for (int32_t q = 0; q < d.nchunk; ++q) {
-            const int64_t r0 = int64_t(q) * kChunkRows;
+    }
+    // Finalisation items (layout.hpp), sized for the set's workgroup.
+    for (const TensorDesc &d : pl.tensors)
+        if (d.kind == KIND_MATRIX && d.nrs > (int64_t(kColLoads) << (kFinSmallLog2 - kMinColsLog2)))
+            pl.fin_log2 = kFinLargeLog2;
+    const int64_t fin_threads = int64_t(1) << pl.fin_log2;
+    const int max_slog = pl.fin_log2 - kMinColsLog2;
+    for (int64_t i = 0; i < count; ++i) {
+        const TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
+        if (d.kind != KIND_MATRIX) continue;
+        // Row items: one row per thread, one partial sum of R per 256 rows.
+        for (int64_t r0 = 0; r0 < d.m; r0 += fin_threads)
             pl.fin.push_back({static_cast<int32_t>(i), FIN_ROWS, static_cast<int32_t>(r0),
-                              static_cast<int32_t>(T.m - r0 < kChunkRows ? T.m - r0 : kChunkRows),
-                              q, 0});
-        }
-        // Column items: 64 columns x one segment of kSegStripes stripes;
-        // tensors with several segments get fold items (second launch).
-        d.nseg = static_cast<int32_t>(ceil_div(d.nrs, kSegStripes));
-        if (d.nseg > 1) {
-            d.colseg = ws;
-            ws += round_up(int64_t(d.nseg) * T.n, 64);
-            for (int64_t j0 = 0; j0 < T.n; j0 += kFoldCols)
-                fold_items.push_back({static_cast<int32_t>(i), FIN_FOLD, static_cast<int32_t>(j0),
-                                      static_cast<int32_t>(T.n - j0 < kFoldCols ? T.n - j0
-                                                                                : kFoldCols),
-                                      0, 0});
-        }
-        for (int32_t q = 0; q < d.nseg; ++q)
-            for (int64_t j0 = 0; j0 < T.n; j0 += kWave)
-                col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
-                                     static_cast<int32_t>(T.n - j0 < kWave ? T.n - j0 : kWave), q,
-                                     0});
+                              static_cast<int32_t>(d.m - r0 < fin_threads ? d.m - r0 : fin_threads),
+                              static_cast<int32_t>(r0 / kChunkRows), 0});
+        // Column items: S stripe lanes x fin_threads / S columns.
+        int slog = 0;
+        while (slog < max_slog && (int64_t(kColLoads) << slog) < d.nrs) ++slog;
+        const int64_t W = fin_threads >> slog;
+        for (int64_t j0 = 0; j0 < d.n; j0 += W)
+            col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
+                                 static_cast<int32_t>(d.n - j0 < W ? d.n - j0 : W), 0, slog});
     }
     // One streaming launch per storage type: its 4-wide matrix tiles, then
     // its one-column matrix tiles (served by the same launch), then its
@@ -319,8 +318,6 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     }
     pl.row_items = static_cast<int64_t>(pl.fin.size());
     pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());
-    pl.fold_items = static_cast<int64_t>(fold_items.size());
-    pl.fin.insert(pl.fin.end(), fold_items.begin(), fold_items.end());
     pl.ws_floats = ws;
     if (pl.tiles.size() > static_cast<size_t>(INT32_MAX) || pl.fin.size() > static_cast<size_t>(INT32_MAX)) {
         err = "parameter set needs more than 2^31 workgroups";

@@ -17,9 +17,9 @@ struct Plan {
     std::vector<Tile> tiles;          // grouped by storage type; see TileGroup
     std::vector<TileGroup> groups;    // one streaming launch each
     int64_t matrix_tiles = 0;
-    std::vector<FinItem> fin;         // row items, column items, then fold items
+    std::vector<FinItem> fin;         // row items, then column items
     int64_t row_items = 0;
-    int64_t fold_items = 0;           // the last fold_items entries: second launch
+    int32_t fin_log2 = kFinSmallLog2; // log2 of the finalisation workgroup size
     int64_t ws_floats = 0;            // partial-sum workspace (floats)
     int64_t matrices = 0, vectors = 0, elements = 0;
     int64_t state_bytes = 0, ikfad_state_bytes = 0, min_bytes = 0, stream_min_bytes = 0;

@@ -114,10 +114,15 @@ static void check_vector_tile(const Plan &pl, const Tile &tl, std::vector<Marks>
 
 static void check_plan(const Plan &pl, int64_t count)
 {
+    // 1024-thread finalisation exactly when some matrix has more row
+    // stripes than 16 stripe lanes of 32 loads cover
+    bool tall = false;
+    for (const TensorDesc &td : pl.tensors)
+        tall = tall || (td.kind == KIND_MATRIX && td.nrs > kColLoads * 16);
+    CHECK(pl.fin_log2 == (tall ? kFinLargeLog2 : kFinSmallLog2), "finalisation workgroup size");
     std::vector<Marks> elems(static_cast<size_t>(count)), rowp(static_cast<size_t>(count)),
         colp(static_cast<size_t>(count)), chunks(static_cast<size_t>(count)),
-        segcols(static_cast<size_t>(count)), folds(static_cast<size_t>(count)),
-        rows(static_cast<size_t>(count));
+        cols(static_cast<size_t>(count)), rows(static_cast<size_t>(count));
     // workspace regions
     std::vector<std::pair<int64_t, int64_t>> regions;
     for (int64_t i = 0; i < count; ++i) {
@@ -127,14 +132,11 @@ static void check_plan(const Plan &pl, int64_t count)
             rowp[static_cast<size_t>(i)].init(int64_t(td.ncb) * td.m);
             colp[static_cast<size_t>(i)].init(int64_t(td.nrs) * td.n);
             chunks[static_cast<size_t>(i)].init(td.nchunk);
-            segcols[static_cast<size_t>(i)].init(int64_t(td.nseg) * td.n);
-            folds[static_cast<size_t>(i)].init(td.nseg > 1 ? td.n : 0);
+            cols[static_cast<size_t>(i)].init(td.n);
             rows[static_cast<size_t>(i)].init(td.m);
             regions.push_back({td.rowpart, int64_t(td.ncb) * td.m});
             regions.push_back({td.colpart, int64_t(td.nrs) * td.n});
             regions.push_back({td.chunk, td.nchunk});
-            if (td.nseg > 1) regions.push_back({td.colseg, int64_t(td.nseg) * td.n});
-            CHECK(td.nseg == (td.nrs + kSegStripes - 1) / kSegStripes, "nseg");
         }
     }
     for (size_t a = 0; a < regions.size(); ++a) {
@@ -178,33 +180,52 @@ static void check_plan(const Plan &pl, int64_t count)
         CHECK(td.kind == KIND_MATRIX, "finalisation item on a vector");
         if (it.kind == FIN_ROWS) {
             CHECK(q < pl.row_items, "row item after the row range");
-            CHECK(it.count >= 1 && it.count <= kChunkRows, "row item count");
+            CHECK(it.count >= 1 && it.count <= (1 << pl.fin_log2), "row item count");
+            CHECK(it.start % kChunkRows == 0 && it.chunk == it.start / kChunkRows,
+                  "row item chunk alignment");
             for (int t = 0; t < it.count; ++t) {
                 rows[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + t, "row item row");
                 for (int cb = 0; cb < td.ncb; ++cb)
                     CHECK(int64_t(cb) * td.m + it.start + t < int64_t(td.ncb) * td.m, "rowpart read");
             }
-            chunks[static_cast<size_t>(it.tensor)].hit(it.chunk, "chunk");
-        } else if (it.kind == FIN_COLS) {
-            CHECK(q >= pl.row_items && q < nfin - pl.fold_items, "column item placement");
-            CHECK(it.count >= 1 && it.count <= kWave && it.chunk < td.nseg, "column item");
-            for (int j = 0; j < it.count; ++j) {
-                segcols[static_cast<size_t>(it.tensor)].hit(int64_t(it.chunk) * td.n + it.start + j,
-                                                             "segment column");
-                const int seg0 = it.chunk * kSegStripes;
-                for (int w = 0; w < 4; ++w) {
-                    const int s0 = std::min(td.nrs, seg0 + w * (kSegStripes / 4));
-                    const int s1 = std::min(td.nrs, s0 + kSegStripes / 4);
-                    for (int s = s0; s < s1; ++s)
-                        CHECK(int64_t(s) * td.n + it.start + j < int64_t(td.nrs) * td.n,
-                              "colpart read");
-                }
-            }
+            // the kernel writes chunk sums for q < kFinThreads / 256 while
+            // q * 256 < count
+            for (int q = 0; q < (1 << pl.fin_log2) / kChunkRows && q * kChunkRows < it.count; ++q)
+                chunks[static_cast<size_t>(it.tensor)].hit(it.chunk + q, "chunk");
         } else {
-            CHECK(it.kind == FIN_FOLD && q >= nfin - pl.fold_items, "fold item placement");
-            CHECK(td.nseg > 1 && it.count >= 1 && it.count <= kFoldCols, "fold item");
-            for (int t = 0; t < it.count; ++t)
-                folds[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + t, "fold column");
+            // Replays the column item: thread (q, c), S stripe lanes x W
+            // columns; every stripe of every column read once, each column
+            // updated once, and stripe lanes enough for at most kColLoads
+            // stripes per thread unless that would leave fewer than 16
+            // columns.
+            CHECK(it.kind == FIN_COLS && q >= pl.row_items, "column item placement");
+            const int slog = it.lanes_log2, max_slog = pl.fin_log2 - kMinColsLog2;
+            CHECK(slog >= 0 && slog <= max_slog, "stripe lanes log2 %d", slog);
+            const int S = 1 << slog, W = (1 << pl.fin_log2) >> slog;
+            CHECK(it.count >= 1 && it.count <= W, "column item count %d W %d", it.count, W);
+            CHECK((int64_t(kColLoads) << slog) >= td.nrs || slog == max_slog,
+                  "stripe lanes too few for %d stripes", td.nrs);
+            CHECK(slog == 0 || (int64_t(kColLoads) << (slog - 1)) < td.nrs,
+                  "stripe lanes more than needed for %d stripes", td.nrs);
+            std::vector<int> seen(static_cast<size_t>(td.nrs) * static_cast<size_t>(W), 0);
+            for (int t = 0; t < (1 << pl.fin_log2); ++t) {
+                const int c = t & (W - 1), lane = t >> (pl.fin_log2 - slog);
+                if (c >= it.count) continue;
+                for (int s0 = lane; s0 < td.nrs; s0 += S * kColLoads)
+                    for (int u = 0; u < kColLoads; ++u) {
+                        const int st = s0 + u * S;
+                        if (st >= td.nrs) continue;
+                        CHECK(int64_t(st) * td.n + it.start + c < int64_t(td.nrs) * td.n,
+                              "colpart read");
+                        seen[static_cast<size_t>(st) * W + c] += 1;
+                    }
+                if (lane == 0) cols[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + c,
+                                                                      "column item column");
+            }
+            for (int st = 0; st < td.nrs; ++st)
+                for (int c = 0; c < it.count; ++c)
+                    CHECK(seen[static_cast<size_t>(st) * W + c] == 1, "stripe %d column %d read %d times",
+                          st, c, seen[static_cast<size_t>(st) * W + c]);
         }
     }
     for (int64_t i = 0; i < count; ++i) {
@@ -216,8 +237,7 @@ static void check_plan(const Plan &pl, int64_t count)
             CHECK(colp[static_cast<size_t>(i)].all(), "column partials incomplete");
             CHECK(chunks[static_cast<size_t>(i)].all(), "chunks incomplete");
             CHECK(rows[static_cast<size_t>(i)].all(), "row items incomplete");
-            CHECK(segcols[static_cast<size_t>(i)].all(), "segment columns incomplete");
-            CHECK(folds[static_cast<size_t>(i)].all(), "fold columns incomplete");
+            CHECK(cols[static_cast<size_t>(i)].all(), "column items incomplete");
         }
     }
 }

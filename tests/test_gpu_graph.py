@@ -19,7 +19,7 @@ S = synth.TensorSpec
 
 @pytest.mark.parametrize("two_pass", [False, True])
 def test_graph_replays_match_eager_bitwise(two_pass):
-    # f: 66 row stripes, two column segments (the second finalisation launch)
+    # f: 66 row stripes (column items of 4 stripe lanes x 64 columns)
     specs = [S("a", 256, 512), S("b", 1, 512), S("c", 300, 27), S("d", 40, 640, "bf16"),
              S("e", 640, 1, "bf16"), S("f", 4200, 96)]
     hp = synth.HP_FRICTION

@@ -80,20 +80,28 @@ def test_edge_shapes(name, specs):
     assert_ok(errs, label=name)
 
 
-SCHEDULE_CASES = [
-    ("tall_segments", [S("a", 9000, 64), S("b", 4200, 96, "bf16")]),
+# Column items split their 256 threads into S stripe lanes x 256 / S
+# columns, S the smallest power of two (<= 64) leaving each thread at most
+# 32 row stripes: S = 1 at 32 stripes (1024 rows), S = 2 at 33 (1056 rows),
+# S = 4 at 66-71 stripes, S = 64 with two batches of loads per thread at
+# 2188 stripes (70000 rows).
+COLUMN_CASES = [
+    ("s1_32_stripes", [S("a", 1024, 300)], 12),
+    ("s2_33_stripes", [S("a", 1056, 300)], 12),
+    ("tall_s4", [S("a", 9000, 64), S("b", 4200, 96, "bf16")], 12),
     ("mixed", [S("a", 96, 200), S("b", 1, 200), S("c", 40, 640, "bf16"), S("d", 640, 1, "bf16"),
-               S("e", 2100, 1000)]),
+               S("e", 2100, 1000)], 12),
+    ("s64_two_batches", [S("a", 70000, 256), S("b", 1, 256)], 5),
 ]
 
 
-@pytest.mark.parametrize("name,specs", SCHEDULE_CASES, ids=[c[0] for c in SCHEDULE_CASES])
-def test_multi_segment_finalisation(name, specs):
-    """Tensors with many row stripes and several column segments (the
-    second, segment-folding finalisation launch) against the oracle, in the
-    friction-active setting, 12 steps."""
-    log(f"[case] multi-segment {name}")
-    _, errs = run_parity(specs, synth.HP_FRICTION, 12, seed=8, label=f"multi-segment {name}")
+@pytest.mark.parametrize("name,specs,steps", COLUMN_CASES, ids=[c[0] for c in COLUMN_CASES])
+def test_column_finalisation(name, specs, steps):
+    """Tensors from a few to thousands of row stripes, across the column
+    items' stripe-lane counts, against the oracle in the friction-active
+    setting."""
+    log(f"[case] column finalisation {name}")
+    _, errs = run_parity(specs, synth.HP_FRICTION, steps, seed=8, label=f"columns {name}")
     assert_ok(errs, label=name)
 
 
@@ -351,7 +359,7 @@ def _run_steps(specs, hp, steps, two_pass=False, seed=5):
 
 
 SPECS_MIX = [S("a", 300, 520), S("b", 1, 520), S("c", 77, 1000, "bf16"), S("d", 129, 27),
-             S("e", 4200, 96)]          # e: 66 row stripes, two column segments
+             S("e", 4200, 96)]          # e: 66 row stripes, 4 stripe lanes per column item
 
 
 def test_deterministic_bitwise():
