@@ -223,6 +223,30 @@ def test_scalar_two_steps_by_hand():
     assert t.x[0, 0] == pytest.approx(0.25 + h * (1 + P1), rel=1e-15)
 
 
+def test_equal_column_factors_damp_each_row_by_its_share():
+    """With every column factor equal, C = c 1, and g = 0, eq. (xi_def) gives
+    row i the same friction c R_i / (1^T R + eps) in every column, so the
+    first half-kick scales row i of P by exp(-(h/2) c R_i / (1^T R + eps)),
+    and the factor update adds kappa times the damped squares' row and
+    column sums.  The factors are seeded unbalanced (1^T R = 6 against
+    1^T C = 4); a run from the paper's zero start keeps 1^T R = 1^T C, so
+    only such a state separates the denominator 1^T R from 1^T C.
+    Catches: denominator summed over C, eps dropped or in the numerator,
+    rows and columns swapped in the factor update."""
+    m, n = 3, 5
+    p0 = _rng(11).standard_normal((m, n))
+    r0, c = np.array([0.5, 2.0, 3.5]), 0.8
+    hp = O.HParams(h=0.6, gamma=0.0, alpha=0.4, mu=0.3, eps_stab=0.25)
+    a, kappa, _ = O.coefficients(hp)
+    t = O.make_tensor(np.zeros((m, n)), p0=p0, r0=r0, c0=np.full(n, c))
+    O.step_list([t], [np.zeros((m, n))], hp)
+    share = c * r0 / (r0.sum() + hp.eps_stab)
+    p1 = p0 * np.exp(-0.5 * hp.h * share)[:, None]
+    np.testing.assert_allclose(t.r, a * r0 + kappa * (p1 ** 2).sum(axis=1), rtol=1e-14)
+    np.testing.assert_allclose(t.c, a * c + kappa * (p1 ** 2).sum(axis=0), rtol=1e-14)
+    np.testing.assert_allclose(t.x, hp.h * p0, rtol=1e-15)
+
+
 # ------------------------------------------------ special cases and identities
 
 @pytest.mark.parametrize("shape", [(1, 9), (11, 1), (1, 1)])
