@@ -124,7 +124,18 @@ rikfad_status rikfad_create(const rikfad_tensor *tensors, int64_t count,
  * fused streaming pass over all tensors (B, A, C.1, the deferred C.4 + D,
  * per-tile row and column partial sums of [P^(1)]^2), the fixed-order
  * finalisation of R, C and 1^T R, and in two-pass mode the C.4 + D pass.
- * Results are bitwise reproducible: no atomics, fixed reduction order. */
+ * Results are bitwise reproducible: no atomics, fixed reduction order.
+ *
+ * HIP graphs: a step only enqueues kernel launches (no allocation, copy,
+ * memset or synchronisation), so it can be captured and replayed.  Whether
+ * a deferred half-kick is pending is host state that the captured launches
+ * bake in: capture after a first eager step, and replay the graph only
+ * while every step goes through it.  rikfad_sync_momentum,
+ * rikfad_set_hparams, rikfad_state_changed and rikfad_step_grads change
+ * that state or the gradient table, so they do not belong between replays
+ * of one graph.  rikfad_step_grads with changed pointers copies the new
+ * table from host memory and may wait for an earlier copy, so it must not
+ * be captured. */
 rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream);
 
 /* As rikfad_step, with new gradient pointers grads[0..count-1] (same shapes,
