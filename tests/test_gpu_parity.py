@@ -80,11 +80,12 @@ def test_edge_shapes(name, specs):
     assert_ok(errs, label=name)
 
 
-# Column items split their 256 threads into S stripe lanes x 256 / S
-# columns, S the smallest power of two (<= 64) leaving each thread at most
-# 32 row stripes: S = 1 at 32 stripes (1024 rows), S = 2 at 33 (1056 rows),
-# S = 4 at 66-71 stripes, S = 64 with two batches of loads per thread at
-# 2188 stripes (70000 rows).
+# Column items split their T threads (256, or 1024 when a matrix has more
+# than 512 row stripes) into S stripe lanes x T / S columns, S the smallest
+# power of two leaving each thread at most 32 row stripes (at least 16
+# columns per item): S = 1 at 32 stripes (1024 rows), S = 2 at 33 (1056
+# rows), S = 4 at 66-71 stripes, S = 64 with two batches of loads per
+# thread at 2188 stripes (70000 rows).
 COLUMN_CASES = [
     ("s1_32_stripes", [S("a", 1024, 300)], 12),
     ("s2_33_stripes", [S("a", 1056, 300)], 12),
@@ -92,6 +93,9 @@ COLUMN_CASES = [
     ("mixed", [S("a", 96, 200), S("b", 1, 200), S("c", 40, 640, "bf16"), S("d", 640, 1, "bf16"),
                S("e", 2100, 1000)], 12),
     ("s64_two_batches", [S("a", 70000, 256), S("b", 1, 256)], 5),
+    # 625 stripes: 1024-thread items of 32 stripe lanes x 32 columns, the
+    # last of 8 columns; the one-column-path matrix shares the launch size
+    ("ragged_1024_threads", [S("a", 20000, 1000), S("b", 300, 27)], 4),
 ]
 
 
