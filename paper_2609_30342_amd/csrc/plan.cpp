@@ -259,24 +259,41 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
 
         int cls = 0;
         while (!(class_dtype[cls] == T.dtype && class_vec[cls] == d.vec)) ++cls;
-        for (int32_t s = 0; s < d.nrs; ++s) {
-            for (int32_t b = 0; b < d.ncb; ++b) {
-                Tile tl{};
-                tl.start = int64_t(s) * stripe_rows;
-                tl.tensor = static_cast<int32_t>(i);
-                tl.count = static_cast<int32_t>(
-                    T.m - tl.start < stripe_rows ? T.m - tl.start : stripe_rows);
-                tl.col0 = blocks[static_cast<size_t>(b)].col0;
-                tl.ncols = blocks[static_cast<size_t>(b)].ncols;
-                tl.stripe = s;
-                tl.cb = b;
-                tl.lanes_log2 = blocks[static_cast<size_t>(b)].llog;
-                tl.kind = KIND_MATRIX;
-                tl.vec = d.vec;
-                tl.dtype = T.dtype;
-                tl.rpw = rpw;
-                mat_tiles[cls].push_back(tl);
+        // Workgroups go to the 8 XCDs round-robin (launch index mod 8).  When
+        // a matrix's last column block is narrow, the tiles of a stripe carry
+        // unequal work, and in stripe-by-stripe order with 2 blocks every
+        // narrow tile would land on the odd XCDs.  In runs of 8 stripes such
+        // a matrix is therefore ordered block by block, so that all blocks of
+        // one stripe lie 8 apart and run on the same XCD.
+        const bool group8 = blocks.back().llog < blocks.front().llog;
+        std::vector<std::pair<int32_t, int32_t>> order;     // (stripe, block)
+        for (int32_t s0 = 0; s0 < d.nrs; s0 += 8) {
+            const int32_t k = d.nrs - s0 < 8 ? d.nrs - s0 : 8;
+            if (group8 && k == 8) {
+                for (int32_t b = 0; b < d.ncb; ++b)
+                    for (int32_t q = 0; q < 8; ++q) order.push_back({s0 + q, b});
+            } else {
+                for (int32_t q = 0; q < k; ++q)
+                    for (int32_t b = 0; b < d.ncb; ++b) order.push_back({s0 + q, b});
             }
+        }
+        for (const std::pair<int32_t, int32_t> &sb : order) {
+            const int32_t s = sb.first, b = sb.second;
+            Tile tl{};
+            tl.start = int64_t(s) * stripe_rows;
+            tl.tensor = static_cast<int32_t>(i);
+            tl.count = static_cast<int32_t>(
+                T.m - tl.start < stripe_rows ? T.m - tl.start : stripe_rows);
+            tl.col0 = blocks[static_cast<size_t>(b)].col0;
+            tl.ncols = blocks[static_cast<size_t>(b)].ncols;
+            tl.stripe = s;
+            tl.cb = b;
+            tl.lanes_log2 = blocks[static_cast<size_t>(b)].llog;
+            tl.kind = KIND_MATRIX;
+            tl.vec = d.vec;
+            tl.dtype = T.dtype;
+            tl.rpw = rpw;
+            mat_tiles[cls].push_back(tl);
         }
     }
     // Finalisation items (layout.hpp), sized for the set's workgroup.

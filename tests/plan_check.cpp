@@ -279,6 +279,41 @@ int main(int argc, char **argv)
           "992x2048 set (248 tiles at full rpw): rpw %d, %lld tiles", single_rpw(992, 2048, &nt),
           (long long)nt);
 
+    {
+        // A matrix whose last column block is narrow (n = 384: 256 + 128
+        // columns) is ordered in runs of 8 stripes block by block, so that
+        // all tiles of a stripe share their launch position mod 8 (one XCD);
+        // 768 columns (three full blocks) keep stripe-by-stripe order.
+        for (int64_t n : {384, 768}) {
+            const uintptr_t b = uintptr_t(1) << 40;
+            rikfad_tensor t{};
+            t.x = reinterpret_cast<void *>(b);
+            t.g = reinterpret_cast<const void *>(b + (uintptr_t(1) << 36));
+            t.p = reinterpret_cast<float *>(b + (uintptr_t(2) << 36));
+            t.r = reinterpret_cast<float *>(b + (uintptr_t(3) << 36));
+            t.c = reinterpret_cast<float *>(b + (uintptr_t(4) << 36));
+            t.m = 2048;
+            t.n = n;
+            t.dtype = RIKFAD_FP32;
+            Plan pl;
+            std::string err;
+            CHECK(plan_rikfad(&t, 1, pl, err) == RIKFAD_OK, "plan 2048x%lld", (long long)n);
+            std::vector<int> residue(static_cast<size_t>(pl.tensors[0].nrs), -1);
+            bool same_xcd = true, stripe_major = true;
+            for (size_t k = 0; k < pl.tiles.size(); ++k) {
+                const Tile &tl = pl.tiles[k];
+                int &r = residue[static_cast<size_t>(tl.stripe)];
+                if (r < 0) r = static_cast<int>(k % 8);
+                same_xcd = same_xcd && r == static_cast<int>(k % 8);
+                stripe_major = stripe_major &&
+                               static_cast<int64_t>(k) == int64_t(tl.stripe) * pl.tensors[0].ncb + tl.cb;
+            }
+            if (n == 384) CHECK(same_xcd, "n = 384: a stripe's tiles on different XCDs");
+            else CHECK(stripe_major, "n = 768: order changed");
+            check_plan(pl, 1);
+        }
+    }
+
     const int trials = argc > 1 ? std::atoi(argv[1]) : 300;
     std::mt19937_64 rng(12345);
     const int64_t dims[] = {1, 2, 3, 4, 5, 7, 8, 12, 16, 27, 31, 33, 63, 64, 65, 100, 127, 128,
