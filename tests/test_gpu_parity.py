@@ -52,6 +52,32 @@ def test_single_matrix_friction_active(gamma):
     assert np.median(0.5 * hp["h"] * xi) > 0.02      # the friction path is exercised
 
 
+# The host folds the hyperparameters into e^{-alpha h}, (1 - e^{-alpha h}) /
+# (mu alpha), e^{-gamma h} and h once per set_hparams (Section 2, the factor
+# filter's exact solution).  Limits of that computation, each with kappa
+# near 1 so the friction stays active:
+COEFF_CASES = [
+    # alpha = 0: the factors integrate (P^(1))^2 without decay, kappa = h / mu
+    ("alpha_0", dict(h=0.1, gamma=0.0, alpha=0.0, mu=0.1, eps_stab=1e-8)),
+    # alpha h = 1e-7: 1 - e^{-alpha h} survives only through expm1, and
+    # e^{-alpha h} is within two fp32 ulps of 1
+    ("alpha_h_1e-7", dict(h=0.1, gamma=0.0, alpha=1e-6, mu=0.1, eps_stab=1e-8)),
+    # strong damping: e^{-gamma h} = e^{-1/2}
+    ("gamma_h_0.5", dict(h=0.1, gamma=5.0, alpha=0.1, mu=0.1, eps_stab=1e-8)),
+]
+
+
+@pytest.mark.parametrize("name,hp", COEFF_CASES, ids=[c[0] for c in COEFF_CASES])
+def test_coefficient_limits(name, hp):
+    specs = [S("a", 300, 520), S("b", 1, 520), S("c", 77, 1000, "bf16"), S("d", 129, 27)]
+    log(f"[case] coefficients {name} hp={hp}")
+    pair, errs = run_parity(specs, hp, 12, seed=11, label=f"coefficients {name}")
+    assert_ok(errs, label=name)
+    o = pair.ref[0]
+    xi = O.rank1_friction(o.r, o.c, hp["eps_stab"])
+    assert np.median(0.5 * hp["h"] * xi) > 0.005     # the friction path is exercised
+
+
 # ------------------------------------------------------- shapes and tails
 
 EDGE = [
