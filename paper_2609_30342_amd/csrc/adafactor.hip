@@ -331,29 +331,39 @@ __global__ __launch_bounds__(kThreads) void adafm_scale_kernel(
 
 // ---------------------------------------------------------------- pass 3
 
+// Row loads in flight per wave in pass 3 (g, x, M per slot), as in the
+// R-iKFAD streaming pass: the factors are read first, then the load of
+// row-load ld + B goes out as soon as row-load ld has been consumed.
+template <typename XT> struct UpdateRing { static constexpr int value = kRingF32; };
+template <> struct UpdateRing<uint16_t> { static constexpr int value = kRingBF16; };
+
 template <typename XT, int V>
 __device__ void update_matrix(const TensorDesc &td, const XT *__restrict__ g, const Tile &tile,
                               const float *__restrict__ ws, float s, const AdaCoeffs &k)
 {
+    constexpr int B = UpdateRing<XT>::value;
     const Lanes t = lanes_of<V>(tile);
-    float fc[V];
-    const float myfr = tile_factors<V>(td, t, ws, fc);
     XT *__restrict__ x = static_cast<XT *>(td.x);
     float *__restrict__ mom = td.p;
     const int64_t n = td.n;
-    for (int ld0 = 0; ld0 < t.nld; ld0 += kBatch) {
-        typename Raw<XT, V>::type gr[kBatch], xr[kBatch];
-        float mv[kBatch][V];
+    typename Raw<XT, V>::type gr[B], xr[B];
+    float mv[B][V];
+    float fc[V];
+    const float myfr = tile_factors<V>(td, t, ws, fc);
+    if (t.nld > 0) {
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int64_t off = row_off(t, (ld0 + u) * t.G + t.seg, n);
+        for (int u = 0; u < B; ++u) {
+            const int64_t off = row_off(t, u * t.G + t.seg, n);
             gr[u] = Raw<XT, V>::load(g + off);
             xr[u] = Raw<XT, V>::load(x + off);
             Io<float, V>::load(mom + off, mv[u]);
         }
+    }
+    for (int ld0 = 0; ld0 < t.nld; ld0 += B) {
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int rl = (ld0 + u) * t.G + t.seg;
+        for (int u = 0; u < B; ++u) {
+            const int ld = ld0 + u;
+            const int rl = ld * t.G + t.seg;
             const float fr = __shfl(myfr, rl & (kWave - 1));
             float gv[V], xv[V];
             Raw<XT, V>::unpack(gr[u], gv);
@@ -368,6 +378,12 @@ __device__ void update_matrix(const TensorDesc &td, const XT *__restrict__ g, co
                 const int64_t off = (t.r0 + rl) * n + t.col;
                 Io<XT, V>::store(x + off, xv);
                 Io<float, V>::store(mom + off, mv[u]);
+            }
+            if (ld + B < t.nld) {
+                const int64_t off = row_off(t, (ld + B) * t.G + t.seg, n);
+                gr[u] = Raw<XT, V>::load(g + off);
+                xr[u] = Raw<XT, V>::load(x + off);
+                Io<float, V>::load(mom + off, mv[u]);
             }
         }
     }

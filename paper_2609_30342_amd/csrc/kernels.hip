@@ -87,10 +87,20 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     XT *__restrict__ x = static_cast<XT *>(td.x);
     float *__restrict__ p = td.p;
 
+    // The factors are read first.  Vector-memory loads complete in issue
+    // order (one counter per wave), so factor loads issued behind the row
+    // loads would hold the first row's arithmetic until every row of the
+    // ring had arrived; read first, they come from L2 and the row loads
+    // overlap the arithmetic from the first row on.
+    float cv[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) cv[i] = colok ? gmem(td.c)[col + i] : 0.f;
+    const float denom = sum_r(ws + td.chunk, td.nchunk) + k.eps;
+    const float myrate = lane < nr ? row_rate(k.kh, gmem(td.r)[r0 + lane], denom) : 0.f;
+
     // Ring of B row loads: the load of row-load ld + B is issued as soon
     // as row-load ld has been consumed, so every wave keeps B
-    // 1 KB requests per stream in flight.  The first loads go out before
-    // the factor sum is read, hiding its latency.
+    // 1 KB requests per stream in flight.
     typename Raw<XT, V>::type xr[B], gr[B];
     float qv[B][V];
     // A lane outside the block's columns reads the block's first column.
@@ -100,12 +110,6 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
         if (nr > 0)
             load_row<XT, V>(x, g, p, r0, n, lcol, colok && u * G + seg < nr, u * G + seg, xr[u],
                             gr[u], qv[u]);
-
-    float cv[V];
-#pragma unroll
-    for (int i = 0; i < V; ++i) cv[i] = colok ? gmem(td.c)[col + i] : 0.f;
-    const float denom = sum_r(ws + td.chunk, td.nchunk) + k.eps;
-    const float myrate = lane < nr ? row_rate(k.kh, gmem(td.r)[r0 + lane], denom) : 0.f;
 
     float acc[V];
 #pragma unroll
