@@ -57,6 +57,17 @@ __device__ __forceinline__ double inv_norm(const double *__restrict__ parts, int
     return s > 0.0 ? 1.0 / sqrt(s) : 0.0;
 }
 
+// t where c holds, else +0.  A bitwise mask rather than a select: a select
+// between a loaded value and 0 is compiled into a branch around the load.
+__device__ __forceinline__ float keep_if(bool c, float t)
+{
+    return __uint_as_float(__float_as_uint(t) & (c ? 0xffffffffu : 0u));
+}
+__device__ __forceinline__ double keep_if(bool c, double t)
+{
+    return __longlong_as_double(__double_as_longlong(t) & (c ? ~0ll : 0ll));
+}
+
 // out[i] = sum_j xi[i, j] * (w ? w[j] * scale : 1) with scale = inv_norm of
 // w's fold partials: one wave per row, lanes stride over the columns, fp64
 // accumulation.
@@ -77,7 +88,8 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int64_t j = j0 + 64 * u;
-            v[u] = j < n ? static_cast<double>(xr[j]) * (w ? gp(w)[j] : 1.0) : 0.0;
+            const int64_t jc = j < n ? j : n - 1;         // in the row; masked below
+            v[u] = keep_if(j < n, static_cast<double>(xr[jc]) * (w ? gp(w)[jc] : 1.0));
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) s += v[u];
@@ -104,26 +116,34 @@ __global__ __launch_bounds__(kT) void power_step_kernel(const float *__restrict_
     __shared__ double l[kT / 64][64 * NC];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const double scale = inv_norm(vparts, nvparts);
+    // Every load below is unconditional, its address clamped into the
+    // tensor and its value masked afterwards: loads inside branches make
+    // the compiler wait for all outstanding loads before each use, which
+    // would empty the ring of row loads at every row.
     double wv[NC], acc[NC];
+    int64_t jc[NC];                     // column, clamped into the row
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
         const int64_t j = lane + 64 * k;
-        wv[k] = j < n ? gp(v)[j] * scale : 0.0;
+        jc[k] = j < n ? j : n - 1;
+        wv[k] = keep_if(j < n, gp(v)[jc[k]] * scale);
         acc[k] = 0.0;
     }
     const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kPowRows + wave * (kPowRows / 4);
     const int64_t r1 = r0 + kPowRows / 4 < m ? r0 + kPowRows / 4 : m;
+    const int64_t rlast = r1 - 1;       // a row of xi (m >= 1), the wave's last if it has rows
+    auto load_row = [&](int64_t row, float (&dst)[NC]) {
+        const int64_t rc = row < r1 ? row : rlast;
+#pragma unroll
+        for (int k = 0; k < NC; ++k) {
+            dst[k] = keep_if(lane + 64 * k < n && row < r1, gp(xi)[rc * n + jc[k]]);
+        }
+    };
     // A ring of kPowRing rows per wave: the loads of row i + kPowRing go out
     // before row i is reduced, so the butterflies overlap the loads.
     float ring[kPowRing][NC];
 #pragma unroll
-    for (int q = 0; q < kPowRing; ++q) {
-#pragma unroll
-        for (int k = 0; k < NC; ++k) {
-            const int64_t j = lane + 64 * k;
-            ring[q][k] = (j < n && r0 + q < r1) ? gp(xi)[(r0 + q) * n + j] : 0.f;
-        }
-    }
+    for (int q = 0; q < kPowRing; ++q) load_row(r0 + q, ring[q]);
     for (int64_t i0 = r0; i0 < r1; i0 += kPowRing) {
 #pragma unroll
         for (int q = 0; q < kPowRing; ++q) {
@@ -131,12 +151,7 @@ __global__ __launch_bounds__(kT) void power_step_kernel(const float *__restrict_
             float a[NC];
 #pragma unroll
             for (int k = 0; k < NC; ++k) a[k] = ring[q][k];
-            const int64_t nx = i + kPowRing;
-#pragma unroll
-            for (int k = 0; k < NC; ++k) {
-                const int64_t j = lane + 64 * k;
-                ring[q][k] = (j < n && nx < r1) ? gp(xi)[nx * n + j] : 0.f;
-            }
+            load_row(i + kPowRing, ring[q]);
             double su = 0.0;
 #pragma unroll
             for (int k = 0; k < NC; ++k) su += static_cast<double>(a[k]) * wv[k];
@@ -176,7 +191,8 @@ __global__ __launch_bounds__(kT) void col_partial_kernel(const float *__restrict
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
             const int64_t i = ib + u;
-            v[u] = i < i1 ? static_cast<double>(gp(xi)[i * n + j]) * (w ? gp(w)[i] : 1.0) : 0.0;
+            const int64_t ic = i < i1 ? i : i1 - 1;       // in the stripe; masked below
+            v[u] = keep_if(i < i1, static_cast<double>(gp(xi)[ic * n + j]) * (w ? gp(w)[ic] : 1.0));
         }
 #pragma unroll
         for (int u = 0; u < 16; ++u) acc += v[u];
