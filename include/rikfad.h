@@ -100,8 +100,9 @@ typedef struct rikfad_ctx rikfad_ctx;
  * B column blocks (256 columns, or 64 on the one-column path) and S row
  * stripes (32 rows; 16 in a set with fewer matrix tiles than the chip has
  * compute units; taller for narrow matrices) -- about 0.14 m n bytes
- * (rikfad_query reports the total).  The tensor array is copied; the
- * buffers it points to are not.  Zero-size tensors (m < 1 or n < 1) are
+ * (rikfad_query reports the total).  The tensors and every stream passed to
+ * the context later must belong to that device.  The tensor array is
+ * copied; the buffers it points to are not.  Zero-size tensors (m < 1 or n < 1) are
  * rejected with RIKFAD_EINVAL.
  *
  * Deferred form (default).  The second friction half-kick and D of step n
