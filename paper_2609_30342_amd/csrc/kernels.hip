@@ -87,11 +87,14 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     XT *__restrict__ x = static_cast<XT *>(td.x);
     float *__restrict__ p = td.p;
 
-    // The factors are read first.  Vector-memory loads complete in issue
-    // order (one counter per wave), so factor loads issued behind the row
-    // loads would hold the first row's arithmetic until every row of the
-    // ring had arrived; read first, they come from L2 and the row loads
-    // overlap the arithmetic from the first row on.
+    // The factors are read before the first row load goes out.  Vector
+    // loads complete in issue order (one counter per wave), so factor loads
+    // issued behind the row loads would hold the first row until the whole
+    // ring had arrived.  Read first, their chain of L2 round trips (tile,
+    // tensor, C, the partial sums of R, R) also staggers when workgroups
+    // start streaming, which the memory queues favour: this order measured
+    // faster than issuing the rows first, and than batching the factor
+    // loads into one round trip.
     float cv[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) cv[i] = colok ? gmem(td.c)[col + i] : 0.f;
@@ -99,8 +102,8 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
     const float myrate = lane < nr ? row_rate(k.kh, gmem(td.r)[r0 + lane], denom) : 0.f;
 
     // Ring of B row loads: the load of row-load ld + B is issued as soon
-    // as row-load ld has been consumed, so every wave keeps B
-    // 1 KB requests per stream in flight.
+    // as row-load ld has been consumed, so a wave keeps up to B 1 KB
+    // requests per stream in flight.
     typename Raw<XT, V>::type xr[B], gr[B];
     float qv[B][V];
     // A lane outside the block's columns reads the block's first column.
