@@ -106,6 +106,39 @@ def test_edge_shapes(name, specs):
     assert_ok(errs, label=name)
 
 
+def _random_set(seed):
+    """2 to 7 tensors of random shape (vectors, narrow and ragged, wide,
+    tall), fp32 or bf16, random hyperparameters, aligned or misaligned."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0x5E7])))
+    specs = []
+    for i in range(int(rng.integers(2, 8))):
+        kind = int(rng.integers(0, 4))
+        if kind == 0:                                    # vector, either orientation
+            k = int(rng.integers(1, 2000))
+            m, n = (1, k) if rng.random() < 0.5 else (k, 1)
+        elif kind == 1:                                  # narrow, often not 4-aligned
+            m, n = int(rng.integers(1, 600)), int(rng.integers(2, 70))
+        elif kind == 2:                                  # wide, ragged last block
+            m, n = int(rng.integers(1, 80)), int(rng.integers(200, 3000))
+        else:                                            # tall: many row stripes
+            m, n = int(rng.integers(600, 5000)), int(rng.integers(2, 300))
+        specs.append(S(f"t{i}", m, n, "bf16" if rng.random() < 0.4 else "fp32"))
+    hp = dict(h=float(rng.choice([1e-3, 0.05, 0.1])), gamma=float(rng.choice([0.0, 0.05])),
+              alpha=float(rng.choice([0.0, 0.1, 0.5])), mu=float(rng.choice([0.1, 1.0])),
+              eps_stab=float(rng.choice([0.0, 1e-8, 0.1])))
+    return specs, hp, int(rng.random() < 0.3)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_sets(seed):
+    """Seeded random parameter sets against the oracle, 6 steps each."""
+    specs, hp, x_offset = _random_set(seed)
+    log(f"[case] random set seed={seed} x_offset={x_offset} hp={hp} "
+        f"{[(s.m, s.n, s.dtype) for s in specs]}")
+    _, errs = run_parity(specs, hp, 6, seed=seed, x_offset=x_offset, label=f"random {seed}")
+    assert_ok(errs, label=f"random {seed}")
+
+
 # Column items split their T threads (256, or 1024 when a matrix has more
 # than 512 row stripes) into S stripe lanes x T / S columns, S the smallest
 # power of two leaving each thread at most 32 row stripes (at least 16
