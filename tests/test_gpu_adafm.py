@@ -49,6 +49,41 @@ def test_options(variant):
     assert_ok(errs, label=variant)
 
 
+def _random_set(seed):
+    """2 to 7 tensors of random shape (vectors, narrow and ragged, wide,
+    tall), fp32 or bf16, random options, aligned or misaligned."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0xADA])))
+    specs = []
+    for i in range(int(rng.integers(2, 8))):
+        kind = int(rng.integers(0, 4))
+        if kind == 0:
+            k = int(rng.integers(1, 2000))
+            m, n = (1, k) if rng.random() < 0.5 else (k, 1)
+        elif kind == 1:
+            m, n = int(rng.integers(1, 600)), int(rng.integers(2, 70))
+        elif kind == 2:
+            m, n = int(rng.integers(1, 80)), int(rng.integers(200, 3000))
+        else:
+            m, n = int(rng.integers(600, 5000)), int(rng.integers(2, 300))
+        specs.append(S(f"t{i}", m, n, "bf16" if rng.random() < 0.4 else "fp32"))
+    hp = dict(h=float(rng.choice([1e-3, 1e-2])), beta1=float(rng.choice([0.0, 0.9])),
+              clip_threshold=float(rng.choice([0.0, 0.5, 1.0])),
+              scale_parameter=bool(rng.random() < 0.5))
+    return specs, hp, int(rng.random() < 0.3), int(rng.choice([1, 1, 50]))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_sets(seed):
+    """Seeded random parameter sets against the oracle, 4 steps each, some
+    starting late in the beta2 schedule."""
+    specs, hp, x_offset, t0 = _random_set(seed)
+    log(f"[case] adafm random set seed={seed} x_offset={x_offset} t0={t0} hp={hp} "
+        f"{[(s.m, s.n, s.dtype) for s in specs]}")
+    _, errs = run_adafm_parity(specs, hp, 4, seed=seed, x_offset=x_offset, first_step=t0,
+                               label=f"random {seed}")
+    assert_ok(errs, label=f"adafm random {seed}")
+
+
 EDGE = [
     ("ragged_n27", [S("a", 300, 27)]),
     ("wide_ragged", [S("a", 257, 1000)]),
