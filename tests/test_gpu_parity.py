@@ -591,36 +591,50 @@ def test_query_reports_state_and_traffic():
 
 # --------------------------------------------------------- full iKFAD
 
-@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_full_ikfad_matches_oracle(dtype):
-    specs = [S("a", 256, 512, dtype), S("b", 1, 100, dtype), S("c", 33, 27, dtype)]
-    hp = synth.HP_FRICTION
-    wl = synth.Workload(specs, seed=9)
-    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    xs = [torch.from_numpy(wl.x0(i)).to(dt).cuda() for i in range(len(specs))]
+def _ikfad_parity(specs, hp, steps, seed):
+    """Full-tensor iKFAD through the library against the oracle's element-wise
+    step; bf16 parameters are reset to the oracle's before every step and
+    compared with its unrounded update."""
+    wl = synth.Workload(specs, seed=seed)
+    dts = [torch.bfloat16 if sp.dtype == "bf16" else torch.float32 for sp in specs]
+    xs = [torch.from_numpy(wl.x0(i)).to(dts[i]).cuda() for i in range(len(specs))]
     gs = [torch.empty_like(x) for x in xs]
-    log(f"[case] full iKFAD {dtype}")
     ik = R.IKFAD(xs, gs, h=hp["h"], gamma=hp["gamma"], alpha=hp["alpha"], mu=hp["mu"])
     ref = []
     for i in range(len(specs)):
         x = wl.x0(i).astype(np.float64).ravel().copy()
         ref.append((x, np.zeros_like(x), np.zeros_like(x), np.zeros_like(x)))
-    for s in range(10):
-        for i in range(len(specs)):
+    for s in range(steps):
+        for i, sp in enumerate(specs):
             g = wl.grad(i, s)
-            if dtype == "bf16":
-                xs[i].copy_(torch.from_numpy(ref[i][0].reshape(xs[i].shape)).to(dt))
-            gs[i].copy_(torch.from_numpy(g).to(dt))
+            if sp.dtype == "bf16":
+                xs[i].copy_(torch.from_numpy(ref[i][0].reshape(xs[i].shape)).to(dts[i]))
+            gs[i].copy_(torch.from_numpy(g).to(dts[i]))
             O.ikfad_step(ref[i][0], g.ravel(), ref[i][1], ref[i][2], O.HParams(**hp),
-                         x_bf16=(dtype == "bf16"), x_unrounded=ref[i][3])
+                         x_bf16=(sp.dtype == "bf16"), x_unrounded=ref[i][3])
         ik.step()
         torch.cuda.synchronize()
-    for i in range(len(specs)):
+    for i, sp in enumerate(specs):
         p, xi = ik.state[i]
-        want_x = ref[i][3] if dtype == "bf16" else ref[i][0]
-        assert rel_rms(host(xs[i]).ravel(), want_x) < (4e-3 if dtype == "bf16" else TOL_F32)
+        bf = sp.dtype == "bf16"
+        assert rel_rms(host(xs[i]).ravel(), ref[i][3] if bf else ref[i][0]) < (4e-3 if bf else TOL_F32)
         assert rel_rms(host(p).ravel(), ref[i][1]) < TOL_F32
         assert rel_plain(host(xi).ravel(), ref[i][2]) < TOL_F32
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_full_ikfad_matches_oracle(dtype):
+    log(f"[case] full iKFAD {dtype}")
+    _ikfad_parity([S("a", 256, 512, dtype), S("b", 1, 100, dtype), S("c", 33, 27, dtype)],
+                  synth.HP_FRICTION, 10, seed=9)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_full_ikfad_random_sets(seed):
+    specs, hp, _ = _random_set(100 + seed)
+    log(f"[case] full iKFAD random set seed={100 + seed} hp={hp} "
+        f"{[(s.m, s.n, s.dtype) for s in specs]}")
+    _ikfad_parity(specs, hp, 5, seed=seed)
 
 
 # ------------------------------------------------------------- probes
