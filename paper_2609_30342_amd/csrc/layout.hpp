@@ -8,6 +8,9 @@
 
 namespace rk {
 
+// The streaming tile's shape and the ring depths can be overridden at build
+// time (-DRK_...) to measure alternatives; the defaults are the fastest
+// measured on MI355X.
 #ifndef RK_STREAM_WAVES
 #define RK_STREAM_WAVES 8
 #endif
@@ -36,6 +39,11 @@ constexpr int kRowsPerWave = RK_ROWS_PER_WAVE;  // rows per wave of a matrix til
 constexpr int kChunkRows = kThreads;            // rows per finalisation item
 constexpr int kSmallSetTiles = 256;             // compute units of the chip
 constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kVecIters
+static_assert(kStreamWaves >= 1 && kStreamWaves <= 16, "a workgroup holds at most 16 waves");
+static_assert(kRingF32 >= 1 && kRingBF16 >= 1, "a ring holds at least one row load");
+static_assert(kRowsPerWave >= 1 && kRowsPerWave <= kMaxRowsPerWave, "rows per wave");
+static_assert(kBlockLanes >= 1 && kBlockLanes <= kWave && (kBlockLanes & (kBlockLanes - 1)) == 0,
+              "a column block is a power of two of lanes, at most one wave");
 
 enum : int32_t { DT_F32 = 0, DT_BF16 = 1 };
 enum : int32_t { KIND_MATRIX = 0, KIND_VECTOR = 1 };
