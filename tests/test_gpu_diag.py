@@ -42,6 +42,11 @@ CASES = [
     ("single_row", lambda: _mixture(1, 300, 1, 6), 0.0),
     ("mixture2_700x1000", lambda: _mixture(700, 1000, 2, 7), 1e-8),    # widest one-pass rows
     ("mixture2_300x1025", lambda: _mixture(300, 1025, 2, 8), 1e-8),    # two-pass iteration
+    # each register width of the one-pass iteration filled exactly, with a
+    # ragged last block of rows
+    ("mixture2_129x256", lambda: _mixture(129, 256, 2, 9), 1e-8),
+    ("mixture2_257x512", lambda: _mixture(257, 512, 2, 10), 0.0),
+    ("mixture3_1000x768", lambda: _mixture(1000, 768, 3, 11), 1e-8),
 ]
 
 
