@@ -153,7 +153,8 @@ int matrix_blocks(int64_t n, int32_t vec, int base, std::vector<Block> &blocks)
 }
 }  // namespace
 
-rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::string &err)
+rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::string &err,
+                          int rows_per_wave)
 {
     if (count < 0 || (count > 0 && !t)) {
         err = "tensor list is NULL or count < 0";
@@ -183,8 +184,8 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     // dependent row loads: halving the rows per wave doubles the tiles and
     // shortens that chain.  Sets that fill the chip keep the full rows per
     // wave, which streams at a higher rate.
-    int rpw_base = kRowsPerWave;
-    {
+    int rpw_base = rows_per_wave > 0 ? rows_per_wave : kRowsPerWave;
+    if (rows_per_wave <= 0) {
         int64_t ntiles = 0;
         std::vector<Block> blocks;
         for (int64_t i = 0; i < count; ++i) {
@@ -195,6 +196,11 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                       ceil_div(T.m, int64_t(kStreamWaves) * rpw);
         }
         if (ntiles < kSmallSetTiles && kRowsPerWave > 1) rpw_base = kRowsPerWave / 2;
+    }
+
+    if (rpw_base > kMaxRowsPerWave) {
+        err = "rows per wave above " + std::to_string(kMaxRowsPerWave);
+        return RIKFAD_EINVAL;
     }
 
     int64_t ws = 0;

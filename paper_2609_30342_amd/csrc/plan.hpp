@@ -27,7 +27,11 @@ struct Plan {
 
 // Validates and plans an R-iKFAD context.  Returns RIKFAD_OK or an error
 // code with a message in `err`.
-rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &out, std::string &err);
+// rows_per_wave > 0 fixes the rows per wave of every matrix tile (narrow
+// blocks still scale it up); 0 takes kRowsPerWave, halved for sets with
+// fewer matrix tiles than the chip has compute units.
+rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &out, std::string &err,
+                          int rows_per_wave = 0);
 
 // Validates and plans a full-tensor iKFAD context (every tensor element-wise).
 rikfad_status plan_ikfad(const ikfad_tensor *t, int64_t count, Plan &out, std::string &err);

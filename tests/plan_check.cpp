@@ -361,6 +361,14 @@ int main(int argc, char **argv)
         if (s != RIKFAD_OK) continue;
         ++planned;
         check_plan(pl, count);
+        // the Adafactor-m update pass plans the same set with 3 rows per wave
+        Plan pu;
+        CHECK(plan_rikfad(ts.data(), count, pu, err, 3) == RIKFAD_OK, "plan (3 rows per wave): %s",
+              err.c_str());
+        check_plan(pu, count);
+        for (const Tile &tl : pu.tiles)
+            if (tl.kind == KIND_MATRIX && tl.lanes_log2 == 6)
+                CHECK(tl.rpw == 3, "full-width tile with %d rows per wave, not 3", tl.rpw);
     }
     std::printf("plan_check: %d plans checked, %d rejected as expected, %d failures\n", planned,
                 rejected, failures);
