@@ -52,26 +52,34 @@ def measured_traffic(dtype):
 
 # The chip's clocks ramp over the first ~20 ms of sustained load (shader
 # clock 2.1 -> 2.38 GHz on MI355X; a GPT2-S step goes from ~516 us in its
-# first ten steps to a steady ~424 us after about fifty) and drop again
-# when it idles, so every side measurement first keeps the GPU busy for
-# WARM_MS; the headline run takes its --warmup steps (default 100, ~42 ms).
+# first ten steps to a steady ~415 us after about fifty) and drop again
+# when it idles.  Every measurement, the headline included, therefore first
+# keeps the GPU busy with the operation it is about to time for WARM_MS
+# (the pre-warm), then makes its `warmup` untimed calls, then times.  In
+# training the optimiser step follows the forward and backward passes,
+# which keep the clocks up; a step timed on a cold chip measures the
+# clock ramp, not the step.
 WARM_MS = 60.0
 
 
 def warm_up(step, count, warm_ms=WARM_MS):
-    """`count` untimed calls of step(), then more until the GPU has been
-    busy for at least warm_ms (synchronising every 8 calls)."""
+    """Pre-warm: calls of step() until the GPU has been busy for at least
+    warm_ms (synchronising every 8 calls); then `count` untimed calls.
+    Returns the pre-warm's milliseconds and number of calls."""
     import torch
+    calls, ms = 0, 0.0
+    if warm_ms > 0:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < warm_ms:
+            for _ in range(8):
+                step()
+            calls += 8
+            torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
     for _ in range(count):
         step()
-    if warm_ms <= 0:
-        return
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    while (time.perf_counter() - t0) * 1e3 < warm_ms:
-        for _ in range(8):
-            step()
-        torch.cuda.synchronize()
+    return ms, calls
 
 
 def build_workload(specs, dtype, seed, device, scales="lognormal"):
@@ -107,7 +115,7 @@ def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0, scales=
     xs, gs = build_workload(specs, dtype, seed, dev, scales)
     opt = R.RIKFAD(xs, gs, two_pass=two_pass, **hp)
     info = opt.query()
-    warm_up(opt.step, warmup, warm_ms)
+    prewarm_ms, prewarm_steps = warm_up(opt.step, warmup, warm_ms)
     # Timed region: exactly `steps` steps, free of timing events.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -132,7 +140,8 @@ def time_rikfad(specs, dtype, hp, steps, warmup, two_pass=False, seed=0, scales=
     del xs, gs
     torch.cuda.empty_cache()
     return dict(ms_per_step=ms / steps, stream_ms=k1 / n, finalize_ms=k2 / n,
-                apply_ms=k3 / n, timed_steps=n, info=info, nonfinite=nonfinite)
+                apply_ms=k3 / n, timed_steps=n, info=info, nonfinite=nonfinite,
+                prewarm_ms=prewarm_ms, prewarm_steps=prewarm_steps)
 
 
 def time_ikfad(specs, hp, steps, warmup, seed=0, dtype="fp32"):
@@ -176,12 +185,26 @@ def time_adafm(specs, dtype, steps, warmup, seed=0, **hp):
     opt.close()
     del xs, gs
     torch.cuda.empty_cache()
+    stats_b, rms_b = adafm_read_pass_bytes(specs, dtype)
     return {"ms_per_step": ms, "params_per_s": sum(s.numel for s in specs) / (ms * 1e-3),
             "hbm_gbps_step": total / (ms * 1e-3) / 1e9, "min_bytes_per_step": total,
             "state_bytes": state,
             "pass_ms": {"stats": stats / n, "finalize": fin / n, "rms_scale": rms / n,
                         "update": upd / n},
+            "stats_gbps": stats_b / (stats / n * 1e-3) / 1e9,
+            "rms_scale_gbps": rms_b / (rms / n * 1e-3) / 1e9,
             "update_gbps": upd_bytes / (upd / n * 1e-3) / 1e9}
+
+
+def adafm_read_pass_bytes(specs, dtype):
+    """Compulsory bytes of Adafactor-m's two read passes (no parameter
+    scaling): the statistics pass reads each matrix's gradient once and a
+    vector's gradient plus its second moment, which it also writes; the RMS
+    pass reads each matrix's gradient once (vectors finish in pass 1)."""
+    es = 2 if dtype == "bf16" else 4
+    mat = sum(s.numel for s in specs if s.m > 1 and s.n > 1)
+    vec = sum(s.numel for s in specs if s.m == 1 or s.n == 1)
+    return es * mat + (es + 8) * vec, es * mat
 
 
 def time_small(specs, hp, steps, warmup, seed=0):
@@ -240,8 +263,22 @@ def time_friction_report(m, n, iters=30, reps=3):
             "gbps": passes * 4.0 * m * n / (ms * 1e-3) / 1e9}
 
 
+def _time_calls(fn, reps):
+    import torch
+    warm_up(fn, 1)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
 def time_probe(nfloat, reps=50):
-    """3-read / 2-write fp32 stream of the same byte count as the step."""
+    """3-read / 2-write fp32 stream of the same byte count as the step, over
+    five separate buffers (d = a + b, e = a * c)."""
     import torch
     from paper_2609_30342_amd import rikfad as R
     bufs = [torch.empty(nfloat, device="cuda:0") for _ in range(5)]
@@ -249,18 +286,43 @@ def time_probe(nfloat, reps=50):
         b.normal_()
     s = torch.cuda.current_stream().cuda_stream
     ptrs = [b.data_ptr() for b in bufs]
-    warm_up(lambda: R.rikfad_probe_stream(*ptrs, nfloat, s), 1)
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        R.rikfad_probe_stream(*ptrs, nfloat, s)
-    b.record()
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / reps
+    ms = _time_calls(lambda: R.rikfad_probe_stream(*ptrs, nfloat, s), reps)
     del bufs
     torch.cuda.empty_cache()
     return 20.0 * nfloat / (ms * 1e-3) / 1e9
+
+
+def time_probe_mix(nelem, dtype, shape, reps=50):
+    """The step's access mix without its arithmetic, in place: read x, g, p
+    and write x, p (20 B per element fp32, 14 B bf16); shape 0 contiguous,
+    shape 1 the streaming kernel's tiles.  GB/s."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = torch.randn(nelem, device="cuda:0").to(dt)
+    g = torch.randn(nelem, device="cuda:0").to(dt)
+    p = torch.randn(nelem, device="cuda:0")
+    code = R.RIKFAD_BF16 if dtype == "bf16" else R.RIKFAD_FP32
+    s = torch.cuda.current_stream().cuda_stream
+    ms = _time_calls(lambda: R.rikfad_probe_mix(x.data_ptr(), g.data_ptr(), p.data_ptr(), nelem,
+                                                code, shape, s), reps)
+    per = 14.0 if dtype == "bf16" else 20.0
+    del x, g, p
+    torch.cuda.empty_cache()
+    return per * nelem / (ms * 1e-3) / 1e9
+
+
+def time_probe_read(nbytes, reps=50):
+    """Read-only stream of nbytes.  GB/s."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    a = torch.randn(nbytes // 4, device="cuda:0")
+    out = torch.zeros(1, device="cuda:0")
+    s = torch.cuda.current_stream().cuda_stream
+    ms = _time_calls(lambda: R.rikfad_probe_read(a.data_ptr(), nbytes, out.data_ptr(), s), reps)
+    del a, out
+    torch.cuda.empty_cache()
+    return nbytes / (ms * 1e-3) / 1e9
 
 
 def cpu_baseline(specs, hp, budget_s):
@@ -309,8 +371,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=100,
-                    help="untimed steps before the timed ones (the clocks ramp over ~20 ms)")
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed steps after the pre-warm and before the timed ones")
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default="fp32")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of oracle time for cpu_baseline (0 = skip)")
@@ -334,11 +396,12 @@ def main():
     hp = dict(synth.HP_BASE)
     specs = synth.gpt2_small(args.dtype)
     N = sum(s.numel for s in specs)
-    main_run = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup, warm_ms=0.0)
+    main_run = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup)
     info = main_run["info"]
     stream_bytes = info["stream_min_bytes"]
     achieved = stream_bytes / (main_run["stream_ms"] * 1e-3) / 1e9
     step_gbps = info["min_bytes_per_step"] / (main_run["ms_per_step"] * 1e-3) / 1e9
+    kernel_sum = main_run["stream_ms"] + main_run["finalize_ms"]
     traffic = measured_traffic(args.dtype)
     out = {
         "metric": METRIC,
@@ -362,9 +425,12 @@ def main():
             "stream_tiles": info["stream_tiles"],
             "finalize_items": info["finalize_items"],
         },
+        "prewarm": {"ms": main_run["prewarm_ms"], "steps": main_run["prewarm_steps"]},
         "hbm_gbps_step": step_gbps,
         "hbm_frac_step": step_gbps / PEAK_GBPS,
-        "kernel_ms": {"stream": main_run["stream_ms"], "finalize": main_run["finalize_ms"]},
+        "kernel_ms": {"stream": main_run["stream_ms"], "finalize": main_run["finalize_ms"],
+                      "sum": kernel_sum},
+        "step_vs_kernel_sum": main_run["ms_per_step"] / kernel_sum,
         "roofline": {
             "bound": "hbm",
             "achieved": achieved,
@@ -375,6 +441,8 @@ def main():
             "kernel": "rikfad_stream_kernel",
             "bytes_per_launch": stream_bytes,
             "launches_timed": main_run["timed_steps"],
+            "step_frac": step_gbps / PEAK_GBPS,
+            "step_bytes": info["min_bytes_per_step"],
         },
         "state_bytes": {"rikfad": info["state_bytes"], "ikfad": info["ikfad_state_bytes"]},
         "nonfinite": main_run["nonfinite"],
@@ -385,7 +453,9 @@ def main():
         r2 = time_rikfad(synth.gpt2_small(other), other, hp, args.steps, args.warmup)
         var[f"rikfad_{other}"] = {
             "ms_per_step": r2["ms_per_step"], "params_per_s": N / (r2["ms_per_step"] * 1e-3),
-            "stream_ms": r2["stream_ms"],
+            "hbm_frac_step": r2["info"]["min_bytes_per_step"] / (r2["ms_per_step"] * 1e-3)
+            / 1e9 / PEAK_GBPS,
+            "stream_ms": r2["stream_ms"], "finalize_ms": r2["finalize_ms"],
             "stream_gbps": r2["info"]["stream_min_bytes"] / (r2["stream_ms"] * 1e-3) / 1e9}
         tp = time_rikfad(specs, args.dtype, hp, args.steps, args.warmup, two_pass=True)
         var["rikfad_two_pass"] = {"ms_per_step": tp["ms_per_step"],
@@ -411,6 +481,33 @@ def main():
             "stream_gbps": rb["info"]["stream_min_bytes"] / (rb["stream_ms"] * 1e-3) / 1e9}
         var["probe_3r2w_gbps"] = time_probe(N)
         var["stream_kernel_vs_probe"] = achieved / var["probe_3r2w_gbps"]
+        # The chip's ceiling for each access mix, measured in the same run:
+        # the step's own mix without arithmetic (contiguous and in the
+        # streaming kernel's tiles) and a read-only stream of the gradient's
+        # fp32 bytes (what Adafactor-m's read passes move).
+        probes = {f"mix_{dt}_{nm}": time_probe_mix(N, dt, sh)
+                  for dt in ("fp32", "bf16") for sh, nm in ((0, "contig"), (1, "tiles"))}
+        probes["read_only"] = time_probe_read(4 * N)
+        var["probes_gbps"] = probes
+        ceil = {dt: max(probes[f"mix_{dt}_contig"], probes[f"mix_{dt}_tiles"],
+                        *( [var["probe_3r2w_gbps"]] if dt == "fp32" else []))
+                for dt in ("fp32", "bf16")}
+        runs = {args.dtype: (main_run, info), other: (r2, r2["info"])}
+        var["vs_ceiling"] = {
+            dt: {"ceiling_gbps": ceil[dt],
+                 "ceiling_frac_of_peak": ceil[dt] / PEAK_GBPS,
+                 "step_over_ceiling_time": (run["ms_per_step"] * 1e-3)
+                 / (inf["min_bytes_per_step"] / (ceil[dt] * 1e9)),
+                 "stream_over_ceiling_time": (run["stream_ms"] * 1e-3)
+                 / (inf["stream_min_bytes"] / (ceil[dt] * 1e9)),
+                 "gate_us": inf["min_bytes_per_step"] / (0.75 * PEAK_GBPS * 1e9) * 1e6,
+                 "step_us": run["ms_per_step"] * 1e3,
+                 "ceiling_us": inf["min_bytes_per_step"] / (ceil[dt] * 1e9) * 1e6}
+            for dt, (run, inf) in runs.items()}
+        for nm in ("adafm_fp32", "adafm_bf16"):
+            var[nm]["read_passes_vs_read_probe"] = {
+                "stats": var[nm]["stats_gbps"] / probes["read_only"],
+                "rms_scale": var[nm]["rms_scale_gbps"] / probes["read_only"]}
         var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {
             "single_256x512_fp32": time_small(synth.single_matrix(), hp, 200, 5),

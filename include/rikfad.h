@@ -351,10 +351,27 @@ void adafm_destroy(adafm_ctx *ctx);
  *   rikfad_probe_copy: dst[i] = src[i] over nbytes (16-byte aligned,
  *     nbytes % 16 == 0), a plain copy of known size for calibrating
  *     hardware byte counters.
+ *   rikfad_probe_mix: the step's own access mix without its arithmetic --
+ *     read x, g (nelem elements of `dtype`, a rikfad_dtype) and p (nelem
+ *     fp32), write x and p: 20 bytes per element for fp32 x/g, 14 for
+ *     bf16.  x <- x + g (fp32) or the bitwise xor of x and g (bf16),
+ *     p <- p / 2.  shape 0: contiguous, 4096 elements per workgroup of 256
+ *     threads, every load of a workgroup before its first store; shape 1:
+ *     the streaming kernel's workgroup (8 waves, each walking 4 rows of
+ *     256 elements with the same ring of row loads).  nelem % 256 == 0;
+ *     x, g 16-byte (fp32) or 8-byte (bf16) aligned, p 16-byte aligned.
+ *   rikfad_probe_read: reads nbytes from src (16-byte aligned, nbytes % 16
+ *     == 0) in four 16-byte loads per lane; writes *out (one float) only in
+ *     the event that a workgroup's sum has one particular NaN bit pattern,
+ *     which finite data never produces -- a read-only stream.
  * ---------------------------------------------------------------------- */
 rikfad_status rikfad_probe_stream(const float *a, const float *b, const float *c,
                                   float *d, float *e, int64_t nfloat, void *stream);
 rikfad_status rikfad_probe_copy(const void *src, void *dst, int64_t nbytes,
+                                void *stream);
+rikfad_status rikfad_probe_mix(void *x, const void *g, float *p, int64_t nelem,
+                               int32_t dtype, int32_t shape, void *stream);
+rikfad_status rikfad_probe_read(const void *src, int64_t nbytes, float *out,
                                 void *stream);
 
 #ifdef __cplusplus

@@ -847,6 +847,34 @@ rikfad_status rikfad_probe_stream(const float *a, const float *b, const float *c
     return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_stream");
 }
 
+rikfad_status rikfad_probe_mix(void *x, const void *g, float *p, int64_t nelem, int32_t dtype,
+                               int32_t shape, void *stream)
+{
+    if (!x || !g || !p || nelem < 0 || nelem % 256 != 0)
+        return fail(RIKFAD_EINVAL, "probe_mix: NULL pointer or nelem not a multiple of 256");
+    if (dtype != RIKFAD_FP32 && dtype != RIKFAD_BF16)
+        return fail(RIKFAD_EDTYPE, "probe_mix: dtype must be RIKFAD_FP32 or RIKFAD_BF16");
+    if (shape != 0 && shape != 1) return fail(RIKFAD_EINVAL, "probe_mix: shape must be 0 or 1");
+    const uintptr_t xg = dtype == RIKFAD_FP32 ? 16 : 8;
+    if (reinterpret_cast<uintptr_t>(x) % xg || reinterpret_cast<uintptr_t>(g) % xg ||
+        reinterpret_cast<uintptr_t>(p) % 16)
+        return fail(RIKFAD_EALIGN, "probe_mix: x, g 16-byte (fp32) or 8-byte (bf16) and p "
+                                   "16-byte aligned");
+    hipError_t err = rk::launch_probe_mix(x, g, p, nelem, dtype, shape,
+                                          static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_mix");
+}
+
+rikfad_status rikfad_probe_read(const void *src, int64_t nbytes, float *out, void *stream)
+{
+    if (!src || !out || nbytes < 0 || nbytes % 16 != 0)
+        return fail(RIKFAD_EINVAL, "probe_read: NULL pointer or nbytes not a multiple of 16");
+    if (reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(out) % 4)
+        return fail(RIKFAD_EALIGN, "probe_read: src must be 16-byte and out 4-byte aligned");
+    hipError_t err = rk::launch_probe_read(src, nbytes, out, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_read");
+}
+
 rikfad_status rikfad_probe_copy(const void *src, void *dst, int64_t nbytes, void *stream)
 {
     auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };

@@ -485,6 +485,118 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(
     }
 }
 
+// The step's own access mix without its arithmetic: per element read x, g
+// (storage type XT) and p (fp32), write x and p -- 20 bytes per element
+// with fp32 x/g, 14 with bf16.  x' = x + g (fp32) or the bitwise xor of
+// the two (bf16), p' = p / 2, so every load feeds a store.  Two shapes:
+//   contiguous: 256 threads, four 4-element accesses per lane, all loads
+//               of the workgroup before its first store (4096 elements);
+//   tiles:      the streaming kernel's workgroup of 8 waves, each wave
+//               walking 4 consecutive 256-element rows (64 lanes x 4
+//               elements) with the same ring of row loads.
+template <typename XT> struct MixOp;
+template <> struct MixOp<float> {
+    typedef f32x4 type;
+    static __device__ __forceinline__ type combine(const type &x, const type &g) { return x + g; }
+};
+template <> struct MixOp<uint16_t> {
+    typedef u32x2 type;
+    static __device__ __forceinline__ type combine(const type &x, const type &g) { return x ^ g; }
+};
+
+template <typename XT>
+__global__ __launch_bounds__(kThreads) void probe_mix_contig_kernel(
+    XT *__restrict__ x, const XT *__restrict__ g, float *__restrict__ p, int64_t n4)
+{
+    typedef typename MixOp<XT>::type V;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * kProbeUnroll + threadIdx.x;
+    V vx[kProbeUnroll], vg[kProbeUnroll];
+    f32x4 vp[kProbeUnroll];
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n4) {
+            vx[u] = ldg(reinterpret_cast<const V *>(x) + i);
+            vg[u] = ldg(reinterpret_cast<const V *>(g) + i);
+            vp[u] = ldg(reinterpret_cast<const f32x4 *>(p) + i);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n4) {
+            stg(reinterpret_cast<V *>(x) + i, MixOp<XT>::combine(vx[u], vg[u]));
+            stg(reinterpret_cast<f32x4 *>(p) + i, vp[u] * 0.5f);
+        }
+    }
+}
+
+constexpr int kProbeRowsPerWave = 4;
+constexpr int kProbeRow4 = kWave;                 // 4-element accesses per 256-element row
+
+template <typename XT>
+__global__ __launch_bounds__(kStreamThreads) void probe_mix_tile_kernel(
+    XT *__restrict__ x, const XT *__restrict__ g, float *__restrict__ p, int64_t nrows)
+{
+    typedef typename MixOp<XT>::type V;
+    constexpr int B = RingDepth<XT>::value;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x >> 6;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kStreamWaves * kProbeRowsPerWave +
+                       static_cast<int64_t>(wave) * kProbeRowsPerWave;
+    const int nr = static_cast<int>(max<int64_t>(0, min<int64_t>(kProbeRowsPerWave, nrows - r0)));
+    V *xv = reinterpret_cast<V *>(x);
+    const V *gv = reinterpret_cast<const V *>(g);
+    f32x4 *pv = reinterpret_cast<f32x4 *>(p);
+    V rx[B], rg[B];
+    f32x4 rp[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+        if (u < nr) {
+            const int64_t o = (r0 + u) * kProbeRow4 + lane;
+            rx[u] = ldg(xv + o);
+            rg[u] = ldg(gv + o);
+            rp[u] = ldg(pv + o);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kProbeRowsPerWave; ++k) {
+        const int s = k % B;
+        if (k < nr) {
+            const int64_t o = (r0 + k) * kProbeRow4 + lane;
+            stg(xv + o, MixOp<XT>::combine(rx[s], rg[s]));
+            stg(pv + o, rp[s] * 0.5f);
+            if (k + B < nr) {
+                const int64_t on = (r0 + k + B) * kProbeRow4 + lane;
+                rx[s] = ldg(xv + on);
+                rg[s] = ldg(gv + on);
+                rp[s] = ldg(pv + on);
+            }
+        }
+    }
+}
+
+// Read-only stream: four 16-byte loads per lane, summed; the sum is stored
+// only if its bits equal a NaN pattern that finite inputs cannot produce,
+// so the loads stay live and the kernel writes nothing in practice.
+constexpr uint32_t kProbeSentinel = 0x7fbadbadu;
+
+__global__ __launch_bounds__(kThreads) void probe_read_kernel(const f32x4 *__restrict__ a,
+                                                              int64_t n16, float *__restrict__ out)
+{
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * kProbeUnroll + threadIdx.x;
+    f32x4 v[kProbeUnroll];
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        v[u] = i < n16 ? ldg(a + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) s += (v[u].x + v[u].y) + (v[u].z + v[u].w);
+    if (__float_as_uint(s) == kProbeSentinel) gmem(out)[0] = s;
+}
+
 // ------------------------------------------------------------- launchers
 
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
@@ -572,6 +684,45 @@ hipError_t launch_probe_stream(const float *a, const float *b, const float *c, f
                        reinterpret_cast<const f32x4 *>(a), reinterpret_cast<const f32x4 *>(b),
                        reinterpret_cast<const f32x4 *>(c), reinterpret_cast<f32x4 *>(d),
                        reinterpret_cast<f32x4 *>(e), n4);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_mix(void *x, const void *g, float *p, int64_t nelem, int dtype,
+                            int shape, hipStream_t stream)
+{
+    if (nelem <= 0) return hipSuccess;
+    if (shape == 0) {
+        const uint32_t grid = probe_grid(nelem / 4);
+        if (dtype == DT_F32)
+            hipLaunchKernelGGL(probe_mix_contig_kernel<float>, dim3(grid), dim3(kThreads), 0,
+                               stream, static_cast<float *>(x), static_cast<const float *>(g), p,
+                               nelem / 4);
+        else
+            hipLaunchKernelGGL(probe_mix_contig_kernel<uint16_t>, dim3(grid), dim3(kThreads), 0,
+                               stream, static_cast<uint16_t *>(x),
+                               static_cast<const uint16_t *>(g), p, nelem / 4);
+    } else {
+        const int64_t nrows = nelem / (4 * kProbeRow4);
+        const int64_t per = int64_t(kStreamWaves) * kProbeRowsPerWave;
+        const dim3 grid(static_cast<uint32_t>((nrows + per - 1) / per));
+        if (dtype == DT_F32)
+            hipLaunchKernelGGL(probe_mix_tile_kernel<float>, grid, dim3(kStreamThreads), 0,
+                               stream, static_cast<float *>(x), static_cast<const float *>(g), p,
+                               nrows);
+        else
+            hipLaunchKernelGGL(probe_mix_tile_kernel<uint16_t>, grid, dim3(kStreamThreads), 0,
+                               stream, static_cast<uint16_t *>(x),
+                               static_cast<const uint16_t *>(g), p, nrows);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_read(const void *a, int64_t nbytes, float *out, hipStream_t stream)
+{
+    const int64_t n16 = nbytes / 16;
+    if (n16 <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_read_kernel, dim3(probe_grid(n16)), dim3(kThreads), 0, stream,
+                       static_cast<const f32x4 *>(a), n16, out);
     return hipGetLastError();
 }
 

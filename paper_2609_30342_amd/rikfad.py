@@ -109,6 +109,8 @@ _SIGNATURES = {
     "adafm_destroy": (None, [_vp]),
     "rikfad_probe_stream": (_st, [_vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "rikfad_probe_copy": (_st, [_vp, _vp, _i64, _vp]),
+    "rikfad_probe_mix": (_st, [_vp, _vp, _vp, _i64, _i32, _i32, _vp]),
+    "rikfad_probe_read": (_st, [_vp, _i64, _vp, _vp]),
 }
 
 
@@ -264,6 +266,15 @@ def rikfad_probe_stream(a, b, c, d, e, nfloat, stream=None):
 
 def rikfad_probe_copy(src, dst, nbytes, stream=None):
     _check(lib().rikfad_probe_copy(src, dst, int(nbytes), stream), "rikfad_probe_copy")
+
+
+def rikfad_probe_mix(x, g, p, nelem, dtype, shape, stream=None):
+    _check(lib().rikfad_probe_mix(x, g, p, int(nelem), int(dtype), int(shape), stream),
+           "rikfad_probe_mix")
+
+
+def rikfad_probe_read(src, nbytes, out, stream=None):
+    _check(lib().rikfad_probe_read(src, int(nbytes), out, stream), "rikfad_probe_read")
 
 
 def adafm_params(h, beta1=0.9, decay_rate=-0.8, eps1=1e-30, eps2=1e-3, clip_threshold=1.0,

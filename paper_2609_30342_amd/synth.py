@@ -120,6 +120,10 @@ HP_BASE = dict(h=1e-3, gamma=0.0, alpha=0.1, mu=1.0, eps_stab=1e-8)
 # Friction strong enough to move the momentum visibly: the median (h/2) xi
 # reaches ~0.1 within tens of steps, so the half-kicks are exercised.
 HP_FRICTION = dict(h=0.1, gamma=0.0, alpha=0.1, mu=0.1, eps_stab=1e-8)
+# Friction that is already active after a few steps (median (h/2) xi~
+# about 0.065 after 5 steps of these gradients), for the full-size sets,
+# which the oracle can follow for only a handful of steps.
+HP_FRICTION_FULL = dict(h=0.1, gamma=0.0, alpha=0.1, mu=0.01, eps_stab=1e-8)
 # The paper's tuned GPT2-S values for R-iKFAD0 (App. Optimal Hyperparameters,
 # Table of optimised hyperparameters; eps_stab from Section 4).
 HP_GPT2S_TUNED = dict(h=0.0918, gamma=0.0, alpha=0.0579, mu=1.3637e-6, eps_stab=1e-16)

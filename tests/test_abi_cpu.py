@@ -138,6 +138,12 @@ def test_probes_validate_arguments():
     assert L.rikfad_probe_copy(BASE, BASE + 64, 17, None) == R.RIKFAD_EINVAL
     assert L.rikfad_probe_copy(BASE + 4, BASE + 64, 32, None) == R.RIKFAD_EALIGN
     assert L.rikfad_probe_stream(BASE, BASE, BASE, BASE, BASE, 6, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_mix(BASE, BASE, BASE, 100, R.RIKFAD_FP32, 0, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_mix(BASE, BASE, BASE, 256, 7, 0, None) == R.RIKFAD_EDTYPE
+    assert L.rikfad_probe_mix(BASE, BASE, BASE, 256, R.RIKFAD_FP32, 2, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_mix(BASE + 8, BASE, BASE, 256, R.RIKFAD_FP32, 0, None) == R.RIKFAD_EALIGN
+    assert L.rikfad_probe_read(BASE, 17, BASE, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_read(BASE + 4, 32, BASE, None) == R.RIKFAD_EALIGN
 
 
 def _specs_to_tensors(specs):
@@ -248,3 +254,4 @@ def test_header_compiles_standalone(lang):
         r = subprocess.run([cc, "-fsyntax-only", "-Wall", "-Wextra", "-Werror", "-x", lang, h],
                            capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
+

@@ -293,6 +293,16 @@ def test_gpt2_nano_fp32(variant):
     assert_ok(errs, label="gpt2_nano")
 
 
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_gpt2_nano_fp32_seeds(seed):
+    """The 50-step base run on three more seeds: the margin of the
+    element-wise bound is known across draws, not from one."""
+    log(f"[case] gpt2_nano base seed={seed}")
+    _, errs = run_parity(synth.gpt2_nano(), synth.HP_BASE, 50, seed=seed,
+                         label=f"gpt2_nano base seed={seed}")
+    assert_ok(errs, label=f"gpt2_nano seed {seed}")
+
+
 def test_gpt2_nano_friction_active():
     log("[case] gpt2_nano friction-active")
     _, errs = run_parity(synth.gpt2_nano(), synth.HP_FRICTION, 30, label="gpt2_nano friction")
@@ -324,6 +334,47 @@ def test_gpt2_small_full_size(dtype):
     log(f"[case] gpt2_small {dtype} checked={len(checked)}")
     _, errs = run_parity(specs, synth.HP_BASE, 3, checked=checked, label=f"gpt2_small {dtype}")
     assert_ok(errs, label="gpt2_small")
+
+
+def _assert_friction_active(pair, hp, floor=0.02):
+    """Every followed tensor's median (h/2) xi is above `floor`, so rows C.1
+    and C.4 of the step act on every element in fp32 (at HP_BASE they round
+    to the identity)."""
+    for i, o in pair.ref.items():
+        xi = o.xi if o.is_vector else O.rank1_friction(o.r, o.c, hp["eps_stab"])
+        med = float(np.median(0.5 * hp["h"] * xi))
+        assert med > floor, f"{pair.specs[i].name}: median (h/2) xi = {med:.3g}"
+
+
+@pytest.mark.parametrize("dtype,gamma", [("fp32", 0.0), ("bf16", 0.05)])
+def test_gpt2_small_full_size_friction_active(dtype, gamma):
+    """The benchmarked GPT2-S set (all 148 tensors in one launch) with the
+    friction active: 6 steps at mu = 0.01, and damping D in the bf16 case.
+    The oracle follows the embeddings, block 0 and some vectors."""
+    specs = synth.gpt2_small(dtype)
+    checked = _gpt2s_checked(specs)
+    hp = dict(synth.HP_FRICTION_FULL, gamma=gamma)
+    log(f"[case] gpt2_small {dtype} friction-active gamma={gamma} checked={len(checked)}")
+    pair, errs = run_parity(specs, hp, 6, checked=checked,
+                            label=f"gpt2_small {dtype} friction")
+    assert_ok(errs, label="gpt2_small friction")
+    _assert_friction_active(pair, hp)
+
+
+def test_distilbert_plus_large_matrices_friction_active():
+    """The 1.5B-parameter set (fp32 DistilBERT part, 32 bf16 matrices of
+    4096 x 11008 / 11008 x 4096), Student-t(3) row scales, friction active
+    (6 steps at mu = 0.01).  The oracle follows the embedding, block 0 and
+    two of the large matrices."""
+    specs = synth.distilbert_stress()
+    names = {"word_emb", "l0.q", "l0.k", "l0.v", "l0.ffn1", "l0.ffn2", "big0", "big1"}
+    checked = [i for i, s in enumerate(specs) if s.name in names]
+    hp = synth.HP_FRICTION_FULL
+    log(f"[case] distilbert+large friction-active checked={len(checked)}")
+    pair, errs = run_parity(specs, hp, 6, scales="student_t", checked=checked,
+                            label="distilbert stress friction")
+    assert_ok(errs, label="distilbert stress friction")
+    _assert_friction_active(pair, hp)
 
 
 def test_distilbert_plus_large_matrices():
@@ -650,3 +701,37 @@ def test_probes_compute_what_they_claim():
     R.rikfad_probe_copy(a.data_ptr(), f.data_ptr(), 4 * n, s)
     torch.cuda.synchronize()
     assert torch.equal(d, a + b) and torch.equal(e, a * c) and torch.equal(f, a)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", [0, 1])
+def test_mix_probe_computes_what_it_claims(dtype, shape):
+    # 1000 rows of 256 elements: several workgroups and a ragged last one
+    # in both shapes (4096 and 8192 elements per workgroup).
+    n = 256 * 1000
+    log(f"[case] probe_mix dtype={dtype} shape={shape} n={n}")
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = torch.randn(n, device="cuda").to(dt)
+    g = torch.randn(n, device="cuda").to(dt)
+    p = torch.randn(n, device="cuda")
+    x0, p0 = x.clone(), p.clone()
+    code = R.RIKFAD_BF16 if dtype == "bf16" else R.RIKFAD_FP32
+    R.rikfad_probe_mix(x.data_ptr(), g.data_ptr(), p.data_ptr(), n, code, shape,
+                       torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    if dtype == "bf16":
+        want = x0.view(torch.int16) ^ g.view(torch.int16)
+        assert torch.equal(x.view(torch.int16), want)
+    else:
+        assert torch.equal(x, x0 + g)
+    assert torch.equal(p, p0 * 0.5)
+
+
+def test_read_probe_reads_without_writing():
+    n = (1 << 20) + 12
+    a = torch.randn(n, device="cuda")
+    out = torch.full((1,), 7.0, device="cuda")
+    R.rikfad_probe_read(a.data_ptr(), 4 * n, out.data_ptr(),
+                        torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert out.item() == 7.0
