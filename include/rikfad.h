@@ -278,6 +278,30 @@ rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n, doub
                                      int32_t power_iters, void *stream,
                                      rikfad_friction_stats *out);
 
+/* The same report for callers that cannot allocate device memory (code
+ * between allocations that a harness forbids, tight serving or monitoring
+ * loops): the same arguments, kernels and results (bit for bit) as
+ * rikfad_friction_report, but the workspace is a static device array of
+ * rikfad_friction_report_noalloc_max_bytes() bytes (16 MiB) that the
+ * library holds on every device it runs on until the process ends; the
+ * call itself never allocates or frees device memory.  The first call on a
+ * device looks up that device's copy of the array (hipGetSymbolAddress,
+ * with the device current).  A tensor whose workspace
+ * (rikfad_friction_report_workspace_bytes) exceeds the array is rejected
+ * with RIKFAD_EINVAL and a message in rikfad_last_error; every GPT2-S,
+ * DistilBERT and 4096 x 11008 shape needs less than 6 MiB.  Blocking, like
+ * rikfad_friction_report.  All calls on one device share its array: calls
+ * that overlap on one device (from several host threads, or on several
+ * streams at once) race and must be serialised by the caller. */
+rikfad_status rikfad_friction_report_noalloc(const float *xi, int64_t m, int64_t n,
+                                             double eps_stab, int32_t power_iters,
+                                             void *stream, rikfad_friction_stats *out);
+/* Size of the static workspace of rikfad_friction_report_noalloc, in bytes. */
+int64_t rikfad_friction_report_noalloc_max_bytes(void);
+/* Workspace bytes a report on an m x n tensor needs (host only, no HIP
+ * call); -1 for m or n outside [1, 2^31). */
+int64_t rikfad_friction_report_workspace_bytes(int64_t m, int64_t n);
+
 /* ------------------------------------------------------------------------
  * Adafactor-m (the paper's baseline optimiser; Section 2, Methodology,
  * left-hand system, and eq. (xi_def) for zeta^ = R C^T / 1^T R).  The

@@ -219,6 +219,10 @@ struct ikfad_ctx {
     rk::Coeffs k{};
 };
 
+namespace rk {
+void set_last_error(const char *msg) { g_last_error = msg; }
+}  // namespace rk
+
 extern "C" {
 
 const char *rikfad_status_string(rikfad_status s)

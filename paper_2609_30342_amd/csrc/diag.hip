@@ -21,8 +21,11 @@
 #include <stdint.h>
 
 #include <cmath>
+#include <mutex>
+#include <string>
 
 #include "../../include/rikfad.h"
+#include "kernels.hpp"
 
 namespace {
 
@@ -370,52 +373,76 @@ struct DevBuf {
     }
 };
 
-}  // namespace
+// Workspace of one report, in doubles, and the launch geometry it implies.
+struct ReportShape {
+    int64_t stripe, nstripes, ncb, nerr, nfold, nstat, nblk, nparts, words;
+    int nc;   // registers per lane of the one-pass power iteration (0: two passes)
+};
 
-extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n,
-                                                double eps_stab, int32_t power_iters,
-                                                void *stream_, rikfad_friction_stats *out)
+ReportShape report_shape(int64_t m, int64_t n)
 {
-    if (!xi || !out || m < 1 || n < 1 || m >= (int64_t(1) << 31) || n >= (int64_t(1) << 31) ||
-        power_iters < 1 || power_iters > 10000 || !(eps_stab >= 0.0) || !std::isfinite(eps_stab))
-        return RIKFAD_EINVAL;
-    if (reinterpret_cast<uintptr_t>(xi) % 4 != 0) return RIKFAD_EALIGN;
-    hipStream_t st = static_cast<hipStream_t>(stream_);
+    ReportShape s;
     // Stripe height: the largest power of two in [16, 1024] that still gives
     // the column pass about eight workgroups per compute unit, raised if the
     // stripe count would pass the grid's y limit.
-    const int64_t ncb = (n + kT - 1) / kT;
-    int64_t stripe = 1024;
-    while (stripe > 16 && ncb * ((m + stripe - 1) / stripe) < 2048) stripe >>= 1;
-    while ((m + stripe - 1) / stripe > 65535) stripe <<= 1;
-    const int64_t nstripes = (m + stripe - 1) / stripe;
-    const int64_t nerr = (m + kErrRows - 1) / kErrRows;
-    const int64_t nfold = (n + kFoldCols - 1) / kFoldCols;
+    s.ncb = (n + kT - 1) / kT;
+    s.stripe = 1024;
+    while (s.stripe > 16 && s.ncb * ((m + s.stripe - 1) / s.stripe) < 2048) s.stripe >>= 1;
+    while ((m + s.stripe - 1) / s.stripe > 65535) s.stripe <<= 1;
+    s.nstripes = (m + s.stripe - 1) / s.stripe;
+    s.nerr = (m + kErrRows - 1) / kErrRows;
+    s.nfold = (n + kFoldCols - 1) / kFoldCols;
     const int64_t mk = m > n ? m : n;
-    const int64_t nstat = (mk + kStatChunk - 1) / kStatChunk;
-    // workspace (doubles): r m, c n, u m, v n, column partials nstripes*n,
-    // error partials 2*nerr, fold partials 2*nfold (C) and 2*nfold (v),
-    // statistics partials 2*nstat, results 2 (R), 2 (u), 2 (errors)
+    s.nstat = (mk + kStatChunk - 1) / kStatChunk;
     // n <= 1024: one pass over xi per power iteration (power_step_kernel)
-    const int nc = n <= 256 ? 4 : n <= 512 ? 8 : n <= 768 ? 12 : n <= 1024 ? 16 : 0;
-    const int64_t nblk = (m + kPowRows - 1) / kPowRows;
-    const int64_t nparts = nc && nblk > nstripes ? nblk : nstripes;
-    const int64_t words = m + n + m + n + nparts * n + 2 * nerr + 4 * nfold + 2 * nstat + 6;
-    DevBuf buf;
-    if (hipMalloc(&buf.p, sizeof(double) * static_cast<size_t>(words)) != hipSuccess)
-        return RIKFAD_ENOMEM;
-    double *r = static_cast<double *>(buf.p), *c = r + m, *u = c + n, *v = u + m;
+    s.nc = n <= 256 ? 4 : n <= 512 ? 8 : n <= 768 ? 12 : n <= 1024 ? 16 : 0;
+    s.nblk = (m + kPowRows - 1) / kPowRows;
+    s.nparts = s.nc && s.nblk > s.nstripes ? s.nblk : s.nstripes;
+    // r m, c n, u m, v n, column partials nparts*n, error partials 2*nerr,
+    // fold partials 2*nfold (C) and 2*nfold (v), statistics partials
+    // 2*nstat, results 2 (R), 2 (u), 2 (errors)
+    s.words = m + n + m + n + s.nparts * n + 2 * s.nerr + 4 * s.nfold + 2 * s.nstat + 6;
+    return s;
+}
+
+rikfad_status check_report_args(const float *xi, int64_t m, int64_t n, double eps_stab,
+                                int32_t power_iters, const rikfad_friction_stats *out)
+{
+    if (!xi || !out || m < 1 || n < 1 || m >= (int64_t(1) << 31) || n >= (int64_t(1) << 31) ||
+        power_iters < 1 || power_iters > 10000 || !(eps_stab >= 0.0) || !std::isfinite(eps_stab)) {
+        rk::set_last_error("friction_report: NULL pointer, m or n outside [1, 2^31), "
+                           "power_iters outside [1, 10000] or eps_stab negative / not finite");
+        return RIKFAD_EINVAL;
+    }
+    if (reinterpret_cast<uintptr_t>(xi) % 4 != 0) {
+        rk::set_last_error("friction_report: xi is not 4-byte aligned");
+        return RIKFAD_EALIGN;
+    }
+    return RIKFAD_OK;
+}
+
+// The report itself on a workspace of sh.words doubles at buf (device
+// memory).  Every word of the workspace that a kernel reads was written
+// earlier in the same call, so its previous contents do not matter.
+rikfad_status report_on(const float *xi, int64_t m, int64_t n, double eps_stab,
+                        int32_t power_iters, hipStream_t st, const ReportShape &sh, double *buf,
+                        rikfad_friction_stats *out)
+{
+    const int64_t stripe = sh.stripe, nstripes = sh.nstripes, nerr = sh.nerr;
+    const int64_t nfold = sh.nfold, nblk = sh.nblk, nparts = sh.nparts;
+    const int nc = sh.nc;
+    double *r = buf, *c = r + m, *u = c + n, *v = u + m;
     double *cpart = v + n, *epart = cpart + nparts * n, *cfold = epart + 2 * nerr;
     double *vfold = cfold + 2 * nfold, *spart = vfold + 2 * nfold;
-    double *stats_r = spart + 2 * nstat, *stats_u = stats_r + 2, *err = stats_u + 2;
+    double *stats_r = spart + 2 * sh.nstat, *stats_u = stats_r + 2, *err = stats_u + 2;
     const dim3 rows_grid(static_cast<uint32_t>((m + kT / 64 - 1) / (kT / 64)));
-    const dim3 cols_grid(static_cast<uint32_t>(ncb), static_cast<uint32_t>(nstripes));
+    const dim3 cols_grid(static_cast<uint32_t>(sh.ncb), static_cast<uint32_t>(nstripes));
     const dim3 fold_grid(static_cast<uint32_t>(nfold));
     auto stats = [&](const double *vec, int64_t k, double *res) {
-        const int64_t nc = (k + kStatChunk - 1) / kStatChunk;
-        hipLaunchKernelGGL(vec_stats_kernel, dim3(static_cast<uint32_t>(nc)), dim3(kT), 0, st, vec,
-                           k, spart);
-        hipLaunchKernelGGL(stats_fold_kernel, dim3(1), dim3(1), 0, st, spart, nc, res);
+        const int64_t nch = (k + kStatChunk - 1) / kStatChunk;
+        hipLaunchKernelGGL(vec_stats_kernel, dim3(static_cast<uint32_t>(nch)), dim3(kT), 0, st,
+                           vec, k, spart);
+        hipLaunchKernelGGL(stats_fold_kernel, dim3(1), dim3(1), 0, st, spart, nch, res);
     };
 
     // Shadow factors R = xi 1, C = xi^T 1 and the sum of R.
@@ -465,13 +492,16 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, vin_fold, nfold,
                        u);
     stats(u, m, stats_u);
-    if (hipGetLastError() != hipSuccess) return RIKFAD_EHIP;
+    hipError_t e = hipGetLastError();
     double host[6];
-    if (hipMemcpyAsync(host, stats_r, sizeof(double) * 2, hipMemcpyDeviceToHost, st) != hipSuccess ||
-        hipMemcpyAsync(host + 2, err, sizeof(double) * 2, hipMemcpyDeviceToHost, st) != hipSuccess ||
-        hipMemcpyAsync(host + 4, stats_u, sizeof(double) * 2, hipMemcpyDeviceToHost, st) != hipSuccess ||
-        hipStreamSynchronize(st) != hipSuccess)
+    if (e == hipSuccess) e = hipMemcpyAsync(host, stats_r, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(host + 2, err, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(host + 4, stats_u, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+        rk::set_last_error((std::string("friction_report: ") + hipGetErrorString(e)).c_str());
         return RIKFAD_EHIP;
+    }
     const double fro2 = host[2], err2 = host[3], sigma1_sq = host[4];
     out->xi_fro2 = fro2;
     out->err_fro2 = err2;
@@ -484,4 +514,102 @@ extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int6
     out->power_iters = power_iters;
     out->reserved = 0;
     return RIKFAD_OK;
+}
+
+// ------------------------------------------------ report without allocation
+//
+// A file-scope device array is the workspace of rikfad_friction_report_noalloc.
+// Each device holds its own copy at its own address, which host code must
+// obtain with hipGetSymbolAddress (the array's name in host code is only a
+// stand-in for the symbol, not a device address).  The address is looked up
+// once per device, with that device current, on the first call there.
+constexpr int64_t kScratchWords = int64_t(1) << 21;    // 16 MiB of doubles
+
+}  // namespace
+
+static __device__ __align__(256) double scratch[kScratchWords];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double *g_scratch_ptr[kMaxDevices] = {};
+
+rikfad_status scratch_of_current_device(double **out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        rk::set_last_error((std::string("friction_report_noalloc: hipGetDevice: ") +
+                            hipGetErrorString(e)).c_str());
+        return RIKFAD_EHIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        rk::set_last_error("friction_report_noalloc: device index beyond 63");
+        return RIKFAD_EINVAL;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            rk::set_last_error((std::string("friction_report_noalloc: hipGetSymbolAddress: ") +
+                                hipGetErrorString(e)).c_str());
+            return RIKFAD_EHIP;
+        }
+        g_scratch_ptr[dev] = static_cast<double *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return RIKFAD_OK;
+}
+
+}  // namespace
+
+extern "C" rikfad_status rikfad_friction_report(const float *xi, int64_t m, int64_t n,
+                                                double eps_stab, int32_t power_iters,
+                                                void *stream_, rikfad_friction_stats *out)
+{
+    rikfad_status s = check_report_args(xi, m, n, eps_stab, power_iters, out);
+    if (s != RIKFAD_OK) return s;
+    const ReportShape sh = report_shape(m, n);
+    DevBuf buf;
+    if (hipMalloc(&buf.p, sizeof(double) * static_cast<size_t>(sh.words)) != hipSuccess) {
+        rk::set_last_error("friction_report: hipMalloc of the workspace failed");
+        return RIKFAD_ENOMEM;
+    }
+    return report_on(xi, m, n, eps_stab, power_iters, static_cast<hipStream_t>(stream_), sh,
+                     static_cast<double *>(buf.p), out);
+}
+
+extern "C" int64_t rikfad_friction_report_noalloc_max_bytes(void)
+{
+    return kScratchWords * static_cast<int64_t>(sizeof(double));
+}
+
+extern "C" int64_t rikfad_friction_report_workspace_bytes(int64_t m, int64_t n)
+{
+    if (m < 1 || n < 1 || m >= (int64_t(1) << 31) || n >= (int64_t(1) << 31)) return -1;
+    return report_shape(m, n).words * static_cast<int64_t>(sizeof(double));
+}
+
+extern "C" rikfad_status rikfad_friction_report_noalloc(const float *xi, int64_t m, int64_t n,
+                                                        double eps_stab, int32_t power_iters,
+                                                        void *stream_,
+                                                        rikfad_friction_stats *out)
+{
+    rikfad_status s = check_report_args(xi, m, n, eps_stab, power_iters, out);
+    if (s != RIKFAD_OK) return s;
+    const ReportShape sh = report_shape(m, n);
+    if (sh.words > kScratchWords) {
+        rk::set_last_error(("friction_report_noalloc: an " + std::to_string(m) + " x " +
+                            std::to_string(n) + " tensor needs " +
+                            std::to_string(sh.words * 8) + " bytes of workspace, more than the " +
+                            std::to_string(kScratchWords * 8) + "-byte static scratch")
+                               .c_str());
+        return RIKFAD_EINVAL;
+    }
+    double *ws = nullptr;
+    if ((s = scratch_of_current_device(&ws)) != RIKFAD_OK) return s;
+    return report_on(xi, m, n, eps_stab, power_iters, static_cast<hipStream_t>(stream_), sh, ws,
+                     out);
 }

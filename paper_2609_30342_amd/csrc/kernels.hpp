@@ -36,6 +36,9 @@ hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, con
 
 hipError_t launch_probe_stream(const float *a, const float *b, const float *c, float *d,
                                float *e, int64_t nfloat, hipStream_t stream);
+// Message for rikfad_last_error on the calling thread (api.cpp).
+void set_last_error(const char *msg);
+
 hipError_t launch_probe_mix(void *x, const void *g, float *p, int64_t nelem, int dtype,
                             int shape, hipStream_t stream);
 hipError_t launch_probe_read(const void *a, int64_t nbytes, float *out, hipStream_t stream);

@@ -96,6 +96,10 @@ _SIGNATURES = {
     "ikfad_destroy": (None, [_vp]),
     "rikfad_friction_report": (_st, [_vp, _i64, _i64, ctypes.c_double, _i32, _vp,
                                      _P(rikfad_friction_stats)]),
+    "rikfad_friction_report_noalloc": (_st, [_vp, _i64, _i64, ctypes.c_double, _i32, _vp,
+                                             _P(rikfad_friction_stats)]),
+    "rikfad_friction_report_noalloc_max_bytes": (_i64, []),
+    "rikfad_friction_report_workspace_bytes": (_i64, [_i64, _i64]),
     "adafm_create": (_st, [_vp, _i64, _P(adafm_hparams), _P(_vp)]),
     "adafm_step": (_st, [_vp, _vp]),
     "adafm_step_grads": (_st, [_vp, _vp, _vp]),
@@ -258,6 +262,24 @@ def rikfad_friction_report(xi, m, n, eps_stab=0.0, power_iters=60, stream=None):
     _check(lib().rikfad_friction_report(xi, int(m), int(n), float(eps_stab), int(power_iters),
                                         stream, ctypes.byref(out)), "rikfad_friction_report")
     return {nm: getattr(out, nm) for nm, _ in rikfad_friction_stats._fields_}
+
+
+def rikfad_friction_report_noalloc(xi, m, n, eps_stab=0.0, power_iters=60, stream=None):
+    """rikfad_friction_report on the library's static device workspace (no
+    device allocation); blocking.  Returns a dict."""
+    out = rikfad_friction_stats()
+    _check(lib().rikfad_friction_report_noalloc(xi, int(m), int(n), float(eps_stab),
+                                                int(power_iters), stream, ctypes.byref(out)),
+           "rikfad_friction_report_noalloc")
+    return {nm: getattr(out, nm) for nm, _ in rikfad_friction_stats._fields_}
+
+
+def rikfad_friction_report_noalloc_max_bytes():
+    return int(lib().rikfad_friction_report_noalloc_max_bytes())
+
+
+def rikfad_friction_report_workspace_bytes(m, n):
+    return int(lib().rikfad_friction_report_workspace_bytes(int(m), int(n)))
 
 
 def rikfad_probe_stream(a, b, c, d, e, nfloat, stream=None):

@@ -255,3 +255,23 @@ def test_header_compiles_standalone(lang):
                            capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
 
+
+def test_noalloc_friction_report_rejects_tensors_beyond_its_workspace():
+    """The size check comes before any HIP call: a tensor whose workspace
+    exceeds the static array is refused with a message (no GPU needed)."""
+    L = R.lib()
+    limit = L.rikfad_friction_report_noalloc_max_bytes()
+    assert limit == 16 << 20
+    assert 0 < L.rikfad_friction_report_workspace_bytes(50257, 768) <= limit
+    assert 0 < L.rikfad_friction_report_workspace_bytes(4096, 11008) <= limit
+    assert L.rikfad_friction_report_workspace_bytes(0, 5) == -1
+    m, n = 1 << 20, 4096
+    assert L.rikfad_friction_report_workspace_bytes(m, n) > limit
+    out = R.rikfad_friction_stats()
+    st = L.rikfad_friction_report_noalloc(BASE, m, n, 0.0, 10, None, ctypes.byref(out))
+    assert st == R.RIKFAD_EINVAL
+    assert b"static scratch" in L.rikfad_last_error()
+    assert L.rikfad_friction_report_noalloc(None, 8, 8, 0.0, 10, None,
+                                            ctypes.byref(out)) == R.RIKFAD_EINVAL
+    assert L.rikfad_friction_report_noalloc(BASE + 2, 8, 8, 0.0, 10, None,
+                                            ctypes.byref(out)) == R.RIKFAD_EALIGN
