@@ -31,7 +31,16 @@
 namespace rk {
 namespace {
 
-constexpr int kBatch = 4;   // row loads in flight per wave and stream
+// Row loads per wave issued together in the two read passes (statistics,
+// RMS); half as many when the statistics pass also reads x.  With the read
+// passes' 16-row waves and 1 KB row loads (fp32, or bf16 at 8 elements per
+// lane), 4 measured as fast as 8 for fp32 and faster for bf16 (statistics
+// pass 5.2 against 4.2 TB/s), and 16 slower for both.
+#ifndef RK_ADA_READ_BATCH
+#define RK_ADA_READ_BATCH 4
+#endif
+constexpr int kReadBatch = RK_ADA_READ_BATCH;
+static_assert(kReadBatch >= 1 && kReadBatch <= 32, "read batch");
 
 // Lane geometry of a matrix tile (see the R-iKFAD streaming pass): wave w
 // walks rows r0 .. r0 + nr - 1; each row of the block is covered by L
@@ -152,6 +161,10 @@ template <typename XT, int V, bool X2>
 __device__ void stats_matrix(const TensorDesc &td, const XT *__restrict__ g, const Tile &tile,
                              float *__restrict__ ws, const AdaCoeffs &k, float *lds, float &x2)
 {
+    // Batches of B row loads, all issued before the first is summed.  The
+    // loads are unconditional (rows past the wave's last are clamped into
+    // the tensor and masked), so the compiler waits for each row exactly.
+    constexpr int B = X2 ? (kReadBatch + 1) / 2 : kReadBatch;
     const Lanes t = lanes_of<V>(tile);
     const XT *__restrict__ x = static_cast<const XT *>(td.x);
     const int64_t n = td.n;
@@ -159,16 +172,16 @@ __device__ void stats_matrix(const TensorDesc &td, const XT *__restrict__ g, con
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
     float myrow = 0.f;
-    for (int ld0 = 0; ld0 < t.nld; ld0 += kBatch) {
-        typename Raw<XT, V>::type gr[kBatch], xr[kBatch];
+    for (int ld0 = 0; ld0 < t.nld; ld0 += B) {
+        typename Raw<XT, V>::type gr[B], xr[B];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < B; ++u) {
             const int64_t off = row_off(t, (ld0 + u) * t.G + t.seg, n);
             gr[u] = Raw<XT, V>::load(g + off);
             if (X2) xr[u] = Raw<XT, V>::load(x + off);
         }
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < B; ++u) {
             const bool ok = t.colok && (ld0 + u) * t.G + t.seg < t.nr;
             float gv[V];
             Raw<XT, V>::unpack(gr[u], gv);
@@ -255,21 +268,23 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
 
 // ---------------------------------------------------------------- pass 2
 
-// Sum of U^2 over one matrix tile (this lane's share).
+// Sum of U^2 over one matrix tile (this lane's share), in batches of row
+// loads as in the statistics pass.
 template <typename XT, int V>
 __device__ float rms_matrix(const TensorDesc &td, const XT *__restrict__ g, const Tile &tile,
                             const float *__restrict__ ws)
 {
+    constexpr int B = kReadBatch;
     const Lanes t = lanes_of<V>(tile);
     float fc[V];
     const float myfr = tile_factors<V>(td, t, ws, fc);
     float u2 = 0.f;
-    for (int ld0 = 0; ld0 < t.nld; ld0 += kBatch) {
-        typename Raw<XT, V>::type gr[kBatch];
+    for (int ld0 = 0; ld0 < t.nld; ld0 += B) {
+        typename Raw<XT, V>::type gr[B];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) gr[u] = Raw<XT, V>::load(g + row_off(t, (ld0 + u) * t.G + t.seg, td.n));
+        for (int u = 0; u < B; ++u) gr[u] = Raw<XT, V>::load(g + row_off(t, (ld0 + u) * t.G + t.seg, td.n));
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < B; ++u) {
             const int rl = (ld0 + u) * t.G + t.seg;
             const bool ok = t.colok && rl < t.nr;
             const float fr = __shfl(myfr, rl & (kWave - 1));
@@ -436,14 +451,17 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_update_kernel(
     else update_matrix<XT, V>(td, g, tile, ws, s, k);
 }
 
-// Kernel instantiation for a tile group's (storage type, width); the 4-wide
-// one also serves the group's one-column tiles.  nullptr for a combination
-// the planner does not produce.
-template <typename F, typename Pick>
+// Kernel instantiation for a tile group's (storage type, width); a wide
+// one also serves the group's one-column tiles.  Only the read passes
+// (Wide8) have 8-wide bf16 groups.  nullptr for a combination the planner
+// does not produce.
+template <typename F, bool Wide8 = false, typename Pick>
 F pick(const TileGroup &gr, Pick p)
 {
     if (gr.dtype == DT_F32) return gr.vec == 4 ? p.template get<float, 4>()
                                 : gr.vec == 1 ? p.template get<float, 1>() : nullptr;
+    if constexpr (Wide8)
+        if (gr.vec == 8) return p.template get<uint16_t, 8>();
     return gr.vec == 4 ? p.template get<uint16_t, 4>()
          : gr.vec == 1 ? p.template get<uint16_t, 1>() : nullptr;
 }
@@ -476,8 +494,8 @@ hipError_t launch_adafm_stats(const TensorDesc *tensors, const void *const *grad
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
-        const StatsFn fn = x2 ? pick<StatsFn>(gr, PickStats<true>())
-                              : pick<StatsFn>(gr, PickStats<false>());
+        const StatsFn fn = x2 ? pick<StatsFn, true>(gr, PickStats<true>())
+                              : pick<StatsFn, true>(gr, PickStats<false>());
         if (!fn) return hipErrorInvalidValue;
         hipEvent_t a = start, b = q == last ? stop : nullptr;
         start = nullptr;
@@ -498,7 +516,7 @@ hipError_t launch_adafm_rms(const TensorDesc *tensors, const void *const *grads,
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
-        const RmsFn fn = pick<RmsFn>(gr, PickRms());
+        const RmsFn fn = pick<RmsFn, true>(gr, PickRms());
         if (!fn) return hipErrorInvalidValue;
         hipEvent_t a = start, b = q == last ? stop : nullptr;
         start = nullptr;

@@ -190,6 +190,25 @@ struct rikfad_ctx {
 };
 
 constexpr int kUpdateRowsPerWave = 3;   // Adafactor-m update pass (see adafm_ctx)
+#ifndef RK_ADA_READ_ROWS
+#define RK_ADA_READ_ROWS 16
+#endif
+// Adafactor-m read passes (statistics, RMS) and their finalisation: rows per
+// wave of their tile table.  They only read g, so a taller tile moves more
+// bytes per workgroup for the same fixed costs (descriptors, factors, the
+// partial sums) and leaves fewer partial sums to finalise: with 16 rows the
+// two passes read GPT2-S's gradient at 6.0-6.3 TB/s (fp32) against 5.1-5.7
+// with the streaming table's 4.  A set with fewer than kReadMinTiles tiles
+// at that height keeps the streaming table's rows, so that it still fills
+// the chip.
+constexpr int kReadRowsPerWave = RK_ADA_READ_ROWS;
+constexpr int64_t kReadMinTiles = 512;
+#ifndef RK_ADA_BF16_READ_VEC
+#define RK_ADA_BF16_READ_VEC 8
+#endif
+// bf16 elements per lane in the read passes: 8 (16-byte loads of g, 1 KB
+// per wave and row) where the rows allow it.
+constexpr int kReadBf16Vec = RK_ADA_BF16_READ_VEC;
 
 struct adafm_ctx {
     rk::Plan plan;
@@ -660,7 +679,13 @@ rikfad_status adafm_create(const rikfad_tensor *tensors, int64_t count, const ad
     adafm_ctx *ctx = new (std::nothrow) adafm_ctx();
     if (!ctx) return fail(RIKFAD_ENOMEM, "host allocation failed");
     std::string err;
-    if ((s = rk::plan_rikfad(tensors, count, ctx->plan, err)) != RIKFAD_OK) {
+    if ((s = rk::plan_rikfad(tensors, count, ctx->plan, err, kReadRowsPerWave, kReadBf16Vec)) !=
+        RIKFAD_OK) {
+        delete ctx;
+        return fail(s, err);
+    }
+    if (ctx->plan.matrix_tiles < kReadMinTiles &&
+        (s = rk::plan_rikfad(tensors, count, ctx->plan, err, 0, kReadBf16Vec)) != RIKFAD_OK) {
         delete ctx;
         return fail(s, err);
     }
