@@ -243,9 +243,9 @@ def time_small(specs, hp, steps, warmup, seed=0):
 
 def time_friction_report(m, n, iters=30, reps=3):
     """Rank-1 friction diagnostic on an m x n friction tensor: ms per call and
-    GB/s on the passes over xi it makes: 3 + 1 reads of 4 m n bytes for the
-    factors, errors and sigma_1, plus one read per power iteration when
-    n <= 1024 (one-pass iteration), two otherwise."""
+    GB/s on the passes over xi it makes, 4 m n bytes each: iters + 2 when
+    n <= 1024 (factors; errors with the first power iteration; one pass per
+    iteration; sigma_1), 2 iters + 4 otherwise."""
     import torch
     from paper_2609_30342_amd import rikfad as R
     gen = torch.Generator(device="cuda:0").manual_seed(7)
@@ -256,7 +256,7 @@ def time_friction_report(m, n, iters=30, reps=3):
     for _ in range(reps):
         R.rikfad_friction_report(xi.data_ptr(), m, n, 1e-16, iters, s)
     ms = (time.perf_counter() - t0) / reps * 1e3
-    passes = 3 + (1 if n <= 1024 else 2) * iters + 1
+    passes = iters + 2 if n <= 1024 else 2 * iters + 4
     del xi
     torch.cuda.empty_cache()
     return {"shape": [m, n], "power_iters": iters, "ms": ms,

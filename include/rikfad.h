@@ -256,11 +256,15 @@ void ikfad_destroy(ikfad_ctx *ctx);
  * Eckart-Young floor sqrt(1 - sigma_1^2 / |xi|_F^2) and the stable rank
  * |xi|_F^2 / sigma_1^2.  All reductions are fp64 in a fixed order.
  * Blocking (waits for `stream`); allocates and frees a temporary device
- * workspace of 8 (2 m + 2 n + n max(ceil(m / s), ceil(m / 128))) bytes plus
- * a little, where the column-sum stripe height s is a power of two in
- * [16, 1024] (larger only for m above 2^20).  For n <= 1024 a power
- * iteration reads xi once, otherwise twice.  m, n < 2^31; EINVAL on bad arguments, ENOMEM if the
- * workspace cannot be allocated, EHIP on a launch or copy failure.
+ * workspace of 8 (2 m + 2 n + n P) bytes plus a little
+ * (rikfad_friction_report_workspace_bytes gives the exact size), where
+ * P = ceil(m / 128) for n <= 1024 and otherwise the number of column-sum
+ * stripes ceil(m / s), s a power of two in [16, 1024] (larger only for m
+ * above 2^20).  For n <= 1024 the report reads xi power_iters + 2 times
+ * (the factors in one pass, the errors with the first power iteration,
+ * sigma_1 in a last pass), otherwise 2 power_iters + 4 times.  m, n < 2^31;
+ * EINVAL on bad arguments, ENOMEM if the workspace cannot be allocated,
+ * EHIP on a launch or copy failure (rikfad_last_error says which).
  * ---------------------------------------------------------------------- */
 typedef struct {
     double xi_fro2;            /* |xi|_F^2 */

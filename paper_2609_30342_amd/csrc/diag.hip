@@ -32,8 +32,13 @@ namespace {
 constexpr int kT = 256;            // threads per workgroup
 constexpr int kStatChunk = 4096;   // elements per workgroup of the vector statistics
 constexpr int kErrRows = 16;       // rows per workgroup of the error pass
-constexpr int kFoldCols = 32;      // columns per workgroup of the column fold
-constexpr int kFoldGroups = 8;     // stripe groups per column of the column fold
+// 4 columns x 64 stripe groups per fold workgroup (6.4 us a fold of 393
+// x 768 partial sums with 8 x 32; 2 x 128 slower again).
+#ifndef RK_DIAG_FOLD_COLS
+#define RK_DIAG_FOLD_COLS 4
+#endif
+constexpr int kFoldCols = RK_DIAG_FOLD_COLS;        // columns per workgroup of the column fold
+constexpr int kFoldGroups = 256 / kFoldCols;        // stripe groups per column of the column fold
 static_assert(kFoldCols * kFoldGroups == 256, "fold workgroup shape");
 
 #define DG __attribute__((address_space(1)))
@@ -101,52 +106,89 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
     if (lane == 0) gp(out)[row] = w ? s * scale : s;
 }
 
-// One power-iteration pass over xi for n <= 64 * NC, reading xi once: a
-// workgroup takes kPowRows rows, each wave a quarter of them in order.  Lane l holds columns l, l + 64, ... of a row in registers; the wave
-// forms u_i = sum_j xi[i, j] v[j] scale (lanes in column order, then the
-// butterfly) and adds xi[i, j] u_i to its column accumulators, rows in
-// order.  The waves' column sums are added in wave order into the
-// workgroup's row of part (folded by col_fold_kernel).
-constexpr int kPowRows = 128;      // rows per workgroup
-constexpr int kPowRing = 3;        // row loads in flight per wave
+// One pass over xi for n <= 64 * NC, reading xi once: a workgroup takes
+// kPowRows rows, each wave a quarter of them in order.  Lane l holds
+// columns l, l + 64, ... of a row in registers; the wave forms the row's
+// weighted sum s_i = sum_j xi[i, j] w_j (lanes in column order, then the
+// butterfly) and adds xi[i, j] times a row weight to its column
+// accumulators, rows in order.  The waves' column sums are added in wave
+// order into the workgroup's row of part (folded by col_fold_kernel), and
+// the per-lane scalar sums into the workgroup's pair of spart.  MODE:
+//   kPassSums      w = 1: writes R_i = s_i; column weight 1, so part holds
+//                  partial column sums of xi (C)
+//   kPassPower     w = v / |v| (scale from v's fold partials): u_i = s_i;
+//                  column weight u_i (xi^T u)
+//   kPassPowerErr  kPassPower, plus spart = (sum xi^2, sum (xi - xi~)^2)
+//                  with xi~_ij = R_i C_j / (1^T R + eps) (0 if that is 0)
+//   kPassNorm      kPassPower, plus spart[0] = sum u_i^2
+// Shape of the one-pass kernels, measured on the 50257 x 768 report (30
+// iterations): 128 rows per workgroup (64: 1.57 ms, 256: 1.34 ms), and
+// the load of row i + 1 issued before row i is reduced (more rows ahead
+// measured slower: 2 rows 1.19-1.21 ms, 3 rows 1.25, 4 rows 1.30, against
+// 1.19 ms).
+#ifndef RK_DIAG_POW_ROWS
+#define RK_DIAG_POW_ROWS 128
+#endif
+#ifndef RK_DIAG_POW_RING
+#define RK_DIAG_POW_RING 1
+#endif
+constexpr int kPowRows = RK_DIAG_POW_ROWS;   // rows per workgroup
+constexpr int kPowRing = RK_DIAG_POW_RING;   // rows loaded ahead per wave
+static_assert(kErrRows <= kPowRows, "the error partials hold one pair per one-pass workgroup");
+enum : int { kPassSums = 0, kPassPower = 1, kPassPowerErr = 2, kPassNorm = 3 };
 
-template <int NC>
-__global__ __launch_bounds__(kT) void power_step_kernel(const float *__restrict__ xi, int64_t m,
-                                                        int64_t n, const double *__restrict__ v,
-                                                        const double *__restrict__ vparts,
-                                                        int64_t nvparts, double *__restrict__ part)
+template <int NC, int MODE>
+__global__ __launch_bounds__(kT) void onepass_kernel(
+    const float *__restrict__ xi, int64_t m, int64_t n, const double *__restrict__ v,
+    const double *__restrict__ vparts, int64_t nvparts, const double *__restrict__ r,
+    const double *__restrict__ c, const double *__restrict__ stats_r, double eps,
+    double *__restrict__ rout, double *__restrict__ part, double *__restrict__ spart)
 {
-    __shared__ double l[kT / 64][64 * NC];
+    constexpr bool kWeighted = MODE != kPassSums;
+    constexpr bool kColumns = true;
+    constexpr bool kErr = MODE == kPassPowerErr;
+    __shared__ double l[kT / 64][kColumns ? 64 * NC : 1];
+    __shared__ double ls[kT / 64][2];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const double scale = inv_norm(vparts, nvparts);
+    const double scale = kWeighted ? inv_norm(vparts, nvparts) : 1.0;
     // Every load below is unconditional, its address clamped into the
     // tensor and its value masked afterwards: loads inside branches make
     // the compiler wait for all outstanding loads before each use, which
     // would empty the ring of row loads at every row.
-    double wv[NC], acc[NC];
-    int64_t jc[NC];                     // column, clamped into the row
+    double wv[NC], cv[NC], acc[NC];
+    int jc[NC];                         // column, clamped into the row
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
-        const int64_t j = lane + 64 * k;
-        jc[k] = j < n ? j : n - 1;
-        wv[k] = keep_if(j < n, gp(v)[jc[k]] * scale);
+        const int j = lane + 64 * k;
+        jc[k] = j < n ? j : static_cast<int>(n - 1);
+        wv[k] = kWeighted ? keep_if(j < n, gp(v)[jc[k]] * scale) : 1.0;
+        cv[k] = kErr ? keep_if(j < n, gp(c)[jc[k]]) : 0.0;
         acc[k] = 0.0;
+    }
+    double inv = 0.0;
+    if (kErr) {
+        const double denom = gp(stats_r)[1] + eps;
+        inv = denom == 0.0 ? 0.0 : 1.0 / denom;
     }
     const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kPowRows + wave * (kPowRows / 4);
     const int64_t r1 = r0 + kPowRows / 4 < m ? r0 + kPowRows / 4 : m;
     const int64_t rlast = r1 - 1;       // a row of xi (m >= 1), the wave's last if it has rows
-    auto load_row = [&](int64_t row, float (&dst)[NC]) {
+    auto load_row = [&](int64_t row, float (&dst)[NC], double &rr) {
         const int64_t rc = row < r1 ? row : rlast;
 #pragma unroll
-        for (int k = 0; k < NC; ++k) {
+        for (int k = 0; k < NC; ++k)
             dst[k] = keep_if(lane + 64 * k < n && row < r1, gp(xi)[rc * n + jc[k]]);
-        }
+        if (kErr) rr = keep_if(row < r1, gp(r)[rc] * inv);
     };
     // A ring of kPowRing rows per wave: the loads of row i + kPowRing go out
-    // before row i is reduced, so the butterflies overlap the loads.
+    // before row i is reduced, so the butterflies overlap the loads.  The
+    // ring is refilled unconditionally (rows past the wave's last are
+    // clamped and masked), so every wait is for exactly one row.
     float ring[kPowRing][NC];
+    double rring[kPowRing];
 #pragma unroll
-    for (int q = 0; q < kPowRing; ++q) load_row(r0 + q, ring[q]);
+    for (int q = 0; q < kPowRing; ++q) load_row(r0 + q, ring[q], rring[q]);
+    double sa = 0.0, sb = 0.0;
     for (int64_t i0 = r0; i0 < r1; i0 += kPowRing) {
 #pragma unroll
         for (int q = 0; q < kPowRing; ++q) {
@@ -154,25 +196,64 @@ __global__ __launch_bounds__(kT) void power_step_kernel(const float *__restrict_
             float a[NC];
 #pragma unroll
             for (int k = 0; k < NC; ++k) a[k] = ring[q][k];
-            load_row(i + kPowRing, ring[q]);
+            const double ri = rring[q];
+            load_row(i + kPowRing, ring[q], rring[q]);
             double su = 0.0;
 #pragma unroll
-            for (int k = 0; k < NC; ++k) su += static_cast<double>(a[k]) * wv[k];
+            for (int k = 0; k < NC; ++k)
+                su += kWeighted ? static_cast<double>(a[k]) * wv[k] : static_cast<double>(a[k]);
             su = wave_sum(su);
             if (i < r1) {
+                if (MODE == kPassSums && lane == 0) gp(rout)[i] = su;
+                if (kColumns) {
 #pragma unroll
-                for (int k = 0; k < NC; ++k) acc[k] += static_cast<double>(a[k]) * su;
+                    for (int k = 0; k < NC; ++k)
+                        acc[k] += kWeighted ? static_cast<double>(a[k]) * su
+                                            : static_cast<double>(a[k]);
+                }
+                if (kErr) {
+#pragma unroll
+                    for (int k = 0; k < NC; ++k) {
+                        const double x = a[k];
+                        const double e = x - ri * cv[k];
+                        sa += x * x;
+                        sb += e * e;
+                    }
+                }
+                if (MODE == kPassNorm && lane == 0) sa += su * su;
             }
         }
     }
+    if (kColumns) {
 #pragma unroll
-    for (int k = 0; k < NC; ++k) l[wave][lane + 64 * k] = acc[k];
+        for (int k = 0; k < NC; ++k) l[wave][lane + 64 * k] = acc[k];
+    }
+    if (kErr || MODE == kPassNorm) {
+        sa = wave_sum(sa);
+        sb = wave_sum(sb);
+        if (lane == 0) {
+            ls[wave][0] = sa;
+            ls[wave][1] = sb;
+        }
+    }
     __syncthreads();
-    for (int64_t j = threadIdx.x; j < n; j += kT) {
-        double s = l[0][j];
+    if (kColumns) {
+        for (int64_t j = threadIdx.x; j < n; j += kT) {
+            double s = l[0][j];
 #pragma unroll
-        for (int w = 1; w < kT / 64; ++w) s += l[w][j];
-        gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
+            for (int w = 1; w < kT / 64; ++w) s += l[w][j];
+            gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
+        }
+    }
+    if ((kErr || MODE == kPassNorm) && threadIdx.x == 0) {
+        double a = ls[0][0], b = ls[0][1];
+#pragma unroll
+        for (int w = 1; w < kT / 64; ++w) {
+            a += ls[w][0];
+            b += ls[w][1];
+        }
+        gp(spart)[2 * blockIdx.x] = a;
+        gp(spart)[2 * blockIdx.x + 1] = b;
     }
 }
 
@@ -205,9 +286,10 @@ __global__ __launch_bounds__(kT) void col_partial_kernel(const float *__restrict
 
 // out[j] = sum_s part[s, j]: a workgroup takes kFoldCols columns, its
 // kFoldGroups thread groups sum consecutive ranges of stripes in stripe
-// order and are added in group order.  The workgroup also writes
-// parts[2 b] = sum of out[j]^2 and parts[2 b + 1] = sum of out[j] over its
-// columns (in column order), the partials inv_norm and the statistics use.
+// order (16 loads in flight, addresses clamped and values masked) and are
+// added in group order.  The workgroup also writes parts[2 b] = sum of
+// out[j]^2 and parts[2 b + 1] = sum of out[j] over its columns (in column
+// order), the partials inv_norm and the statistics use.
 __global__ __launch_bounds__(kT) void col_fold_kernel(const double *__restrict__ part, int64_t n,
                                                       int64_t nstripes, double *__restrict__ out,
                                                       double *__restrict__ parts)
@@ -215,31 +297,37 @@ __global__ __launch_bounds__(kT) void col_fold_kernel(const double *__restrict__
     __shared__ double l[kT];
     const int c = threadIdx.x % kFoldCols, g = threadIdx.x / kFoldCols;
     const int64_t j = static_cast<int64_t>(blockIdx.x) * kFoldCols + c;
+    const int64_t jc = j < n ? j : n - 1;
     const int64_t per = (nstripes + kFoldGroups - 1) / kFoldGroups;
     const int64_t s0 = g * per < nstripes ? g * per : nstripes;
     const int64_t s1 = s0 + per < nstripes ? s0 + per : nstripes;
     double acc = 0.0;
-    if (j < n) {
-        for (int64_t b = s0; b < s1; b += 16) {
-            double v[16];
+    for (int64_t b = s0; b < s1; b += 16) {
+        double v[16];
 #pragma unroll
-            for (int u = 0; u < 16; ++u) v[u] = b + u < s1 ? gp(part)[(b + u) * n + j] : 0.0;
-#pragma unroll
-            for (int u = 0; u < 16; ++u) acc += v[u];
+        for (int u = 0; u < 16; ++u) {
+            const int64_t s = b + u < s1 ? b + u : s1 - 1;
+            v[u] = keep_if(b + u < s1 && j < n, gp(part)[s * n + jc]);
         }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += v[u];
     }
     l[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x < kFoldCols) {
+        double v = l[threadIdx.x];
+        for (int gg = 1; gg < kFoldGroups; ++gg) v += l[gg * kFoldCols + threadIdx.x];
+        l[threadIdx.x] = v;
+        if (j < n) gp(out)[j] = v;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
         double q2 = 0.0, q1 = 0.0;
         for (int cc = 0; cc < kFoldCols; ++cc) {
             const int64_t jj = static_cast<int64_t>(blockIdx.x) * kFoldCols + cc;
             if (jj >= n) break;
-            double v = l[cc];
-            for (int gg = 1; gg < kFoldGroups; ++gg) v += l[gg * kFoldCols + cc];
-            gp(out)[jj] = v;
-            q2 += v * v;
-            q1 += v;
+            q2 += l[cc] * l[cc];
+            q1 += l[cc];
         }
         gp(parts)[2 * blockIdx.x] = q2;
         gp(parts)[2 * blockIdx.x + 1] = q1;
@@ -295,7 +383,10 @@ __global__ void stats_fold_kernel(const double *__restrict__ part, int64_t nchun
 }
 
 // Per workgroup of kErrRows rows: sum xi^2 and sum (xi - R_i C_j / (S + eps))^2
-// with S = stats_r[1] (the sum of R) and xi~ = 0 when S + eps == 0.
+// with S = stats_r[1] (the sum of R) and xi~ = 0 when S + eps == 0.  A
+// thread takes columns j = t, t + 256, ...; for each it loads the column's
+// kErrRows entries together (rows clamped into the tensor and masked) and
+// adds them in row order.
 __global__ __launch_bounds__(kT) void err_partial_kernel(const float *__restrict__ xi, int64_t m,
                                                          int64_t n, const double *__restrict__ r,
                                                          const double *__restrict__ c,
@@ -307,14 +398,25 @@ __global__ __launch_bounds__(kT) void err_partial_kernel(const float *__restrict
     const double inv = denom == 0.0 ? 0.0 : 1.0 / denom;
     const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kErrRows;
     const int64_t i1 = i0 + kErrRows < m ? i0 + kErrRows : m;
+    double ri[kErrRows];
+    int64_t ic[kErrRows];
+#pragma unroll
+    for (int u = 0; u < kErrRows; ++u) {
+        ic[u] = i0 + u < i1 ? i0 + u : i1 - 1;
+        ri[u] = keep_if(i0 + u < i1, gp(r)[ic[u]] * inv);
+    }
     double sa = 0.0, sb = 0.0;
-    for (int64_t i = i0; i < i1; ++i) {
-        const double ri = gp(r)[i] * inv;
-        for (int64_t j = threadIdx.x; j < n; j += kT) {
-            const double v = gp(xi)[i * n + j];
-            const double d = v - ri * gp(c)[j];
-            sa += v * v;
-            sb += d * d;
+    for (int64_t j = threadIdx.x; j < n; j += kT) {
+        const double cj = gp(c)[j];
+        float v[kErrRows];
+#pragma unroll
+        for (int u = 0; u < kErrRows; ++u) v[u] = keep_if(i0 + u < i1, gp(xi)[ic[u] * n + j]);
+#pragma unroll
+        for (int u = 0; u < kErrRows; ++u) {
+            const double x = v[u];
+            const double e = x - ri[u] * cj;
+            sa += x * x;
+            sb += e * e;
         }
     }
     sa = wave_sum(sa);
@@ -394,10 +496,11 @@ ReportShape report_shape(int64_t m, int64_t n)
     s.nfold = (n + kFoldCols - 1) / kFoldCols;
     const int64_t mk = m > n ? m : n;
     s.nstat = (mk + kStatChunk - 1) / kStatChunk;
-    // n <= 1024: one pass over xi per power iteration (power_step_kernel)
+    // n <= 1024: xi's rows fit the registers of a wave, and every pass over
+    // xi is one onepass_kernel launch
     s.nc = n <= 256 ? 4 : n <= 512 ? 8 : n <= 768 ? 12 : n <= 1024 ? 16 : 0;
     s.nblk = (m + kPowRows - 1) / kPowRows;
-    s.nparts = s.nc && s.nblk > s.nstripes ? s.nblk : s.nstripes;
+    s.nparts = s.nc ? s.nblk : s.nstripes;
     // r m, c n, u m, v n, column partials nparts*n, error partials 2*nerr,
     // fold partials 2*nfold (C) and 2*nfold (v), statistics partials
     // 2*nstat, results 2 (R), 2 (u), 2 (errors)
@@ -419,6 +522,19 @@ rikfad_status check_report_args(const float *xi, int64_t m, int64_t n, double ep
         return RIKFAD_EALIGN;
     }
     return RIKFAD_OK;
+}
+
+template <int MODE, typename... Args>
+void launch_onepass(int nc, dim3 grid, hipStream_t st, Args... args)
+{
+    if (nc == 4)
+        hipLaunchKernelGGL((onepass_kernel<4, MODE>), grid, dim3(kT), 0, st, args...);
+    else if (nc == 8)
+        hipLaunchKernelGGL((onepass_kernel<8, MODE>), grid, dim3(kT), 0, st, args...);
+    else if (nc == 12)
+        hipLaunchKernelGGL((onepass_kernel<12, MODE>), grid, dim3(kT), 0, st, args...);
+    else
+        hipLaunchKernelGGL((onepass_kernel<16, MODE>), grid, dim3(kT), 0, st, args...);
 }
 
 // The report itself on a workspace of sh.words doubles at buf (device
@@ -445,59 +561,73 @@ rikfad_status report_on(const float *xi, int64_t m, int64_t n, double eps_stab,
         hipLaunchKernelGGL(stats_fold_kernel, dim3(1), dim3(1), 0, st, spart, nch, res);
     };
 
-    // Shadow factors R = xi 1, C = xi^T 1 and the sum of R.
-    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, nullptr, nullptr,
-                       int64_t(0), r);
-    hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, nullptr,
-                       cpart);
-    hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, c, cfold);
-    stats(r, m, stats_r);
-    // |xi|_F^2 and |xi - xi~|_F^2
-    hipLaunchKernelGGL(err_partial_kernel, dim3(static_cast<uint32_t>(nerr)), dim3(kT), 0, st, xi,
-                       m, n, r, c, stats_r, eps_stab, epart);
-    hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(kT), 0, st, epart, nerr, err);
-    // Power iteration on xi^T xi from v = C / |C|: u = xi v / |v|, v <- xi^T u;
-    // each row pass normalises its input from the fold partials of the last
-    // column pass.
-    const double *vin = c, *vin_fold = cfold;
-    const dim3 pow_grid(static_cast<uint32_t>(nblk));
-    for (int it = 0; it < power_iters; ++it) {
-        if (nc) {
-            if (nc == 4)
-                hipLaunchKernelGGL(power_step_kernel<4>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
-                                   vin_fold, nfold, cpart);
-            else if (nc == 8)
-                hipLaunchKernelGGL(power_step_kernel<8>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
-                                   vin_fold, nfold, cpart);
-            else if (nc == 12)
-                hipLaunchKernelGGL(power_step_kernel<12>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
-                                   vin_fold, nfold, cpart);
-            else
-                hipLaunchKernelGGL(power_step_kernel<16>, pow_grid, dim3(kT), 0, st, xi, m, n, vin,
-                                   vin_fold, nfold, cpart);
+    if (nc) {
+        // n <= 1024: iters + 2 passes over xi.  The first forms R = xi 1 and
+        // C = xi^T 1; the first power iteration (from v = C / |C|) also sums
+        // |xi|_F^2 and |xi - xi~|_F^2; the last pass forms |xi v| for the
+        // final unit vector v.
+        const dim3 grid(static_cast<uint32_t>(nblk));
+        launch_onepass<kPassSums>(nc, grid, st, xi, m, n, nullptr, nullptr, 0, nullptr, nullptr,
+                                  nullptr, 0.0, r, cpart, nullptr);
+        hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nblk, c, cfold);
+        stats(r, m, stats_r);
+        const double *vin = c, *vin_fold = cfold;
+        for (int it = 0; it < power_iters; ++it) {
+            if (it == 0) {
+                launch_onepass<kPassPowerErr>(nc, grid, st, xi, m, n, vin, vin_fold, nfold, r, c,
+                                              stats_r, eps_stab, nullptr, cpart, epart);
+                hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(kT), 0, st, epart, nblk, err);
+            } else {
+                launch_onepass<kPassPower>(nc, grid, st, xi, m, n, vin, vin_fold, nfold, nullptr,
+                                           nullptr, nullptr, 0.0, nullptr, cpart, nullptr);
+            }
             hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nblk, v,
                                vfold);
-        } else {
+            vin = v;
+            vin_fold = vfold;
+        }
+        launch_onepass<kPassNorm>(nc, grid, st, xi, m, n, vin, vin_fold, nfold, nullptr, nullptr,
+                                  nullptr, 0.0, nullptr, cpart, epart);
+        hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(kT), 0, st, epart, nblk, stats_u);
+    } else {
+        // Shadow factors R = xi 1, C = xi^T 1 and the sum of R.
+        hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, nullptr,
+                           nullptr, int64_t(0), r);
+        hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe,
+                           nullptr, cpart);
+        hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, c,
+                           cfold);
+        stats(r, m, stats_r);
+        // |xi|_F^2 and |xi - xi~|_F^2
+        hipLaunchKernelGGL(err_partial_kernel, dim3(static_cast<uint32_t>(nerr)), dim3(kT), 0, st,
+                           xi, m, n, r, c, stats_r, eps_stab, epart);
+        hipLaunchKernelGGL(err_fold_kernel, dim3(1), dim3(kT), 0, st, epart, nerr, err);
+        // Power iteration on xi^T xi from v = C / |C|: u = xi v / |v|,
+        // v <- xi^T u; each row pass normalises its input from the fold
+        // partials of the last column pass.
+        const double *vin = c, *vin_fold = cfold;
+        for (int it = 0; it < power_iters; ++it) {
             hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin,
                                vin_fold, nfold, u);
-            hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe, u,
-                               cpart);
-            hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes, v,
-                               vfold);
+            hipLaunchKernelGGL(col_partial_kernel, cols_grid, dim3(kT), 0, st, xi, m, n, stripe,
+                               u, cpart);
+            hipLaunchKernelGGL(col_fold_kernel, fold_grid, dim3(kT), 0, st, cpart, n, nstripes,
+                               v, vfold);
+            vin = v;
+            vin_fold = vfold;
         }
-        vin = v;
-        vin_fold = vfold;
+        // sigma_1 = |xi v| for the final unit vector v.
+        hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin,
+                           vin_fold, nfold, u);
+        stats(u, m, stats_u);
     }
-    // sigma_1 = |xi v| for the final unit vector v.
-    hipLaunchKernelGGL(row_reduce_kernel, rows_grid, dim3(kT), 0, st, xi, m, n, vin, vin_fold, nfold,
-                       u);
-    stats(u, m, stats_u);
+    // stats_r, stats_u and err are adjacent: one copy brings all three back
+    // (host[] keeps the order R, errors, u).
     hipError_t e = hipGetLastError();
-    double host[6];
-    if (e == hipSuccess) e = hipMemcpyAsync(host, stats_r, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipMemcpyAsync(host + 2, err, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipMemcpyAsync(host + 4, stats_u, sizeof(double) * 2, hipMemcpyDeviceToHost, st);
+    double res[6];
+    if (e == hipSuccess) e = hipMemcpyAsync(res, stats_r, sizeof(res), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
+    const double host[6] = {res[0], res[1], res[4], res[5], res[2], res[3]};
     if (e != hipSuccess) {
         rk::set_last_error((std::string("friction_report: ") + hipGetErrorString(e)).c_str());
         return RIKFAD_EHIP;
