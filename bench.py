@@ -234,11 +234,23 @@ def time_small(specs, hp, steps, warmup, seed=0):
     torch.cuda.synchronize()
     graph = a.elapsed_time(b) / steps
     n = sum(sp.numel for sp in specs)
+    info = opt.query()
     opt.close()
     del g, xs, gs
     torch.cuda.empty_cache()
+    best = min(eager, graph)
+    # The ceiling at this size: the step's access mix without arithmetic,
+    # in the streaming kernel's tiles, over the same number of elements of
+    # the set's storage type (one launch, no finalisation).
+    dt = "bf16" if all(sp.dtype == "bf16" for sp in specs) else "fp32"
+    nel = (n // 256) * 256
+    probe_gbps = time_probe_mix(nel, dt, 1, reps=200)
     return {"params": n, "eager_us": eager * 1e3, "graph_us": graph * 1e3,
-            "graph_params_per_s": n / (graph * 1e-3)}
+            "graph_params_per_s": n / (graph * 1e-3),
+            "min_bytes_per_step": info["min_bytes_per_step"],
+            "hbm_frac_step": info["min_bytes_per_step"] / (best * 1e-3) / 1e9 / PEAK_GBPS,
+            "probe_mix_tiles_us": info["min_bytes_per_step"] / (probe_gbps * 1e9) * 1e6,
+            "probe_mix_tiles_frac": probe_gbps / PEAK_GBPS}
 
 
 def time_friction_report(m, n, iters=30, reps=3):

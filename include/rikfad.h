@@ -189,8 +189,9 @@ rikfad_status rikfad_state_bytes(const rikfad_tensor *tensors, int64_t count,
                                  int64_t *rikfad_bytes, int64_t *ikfad_bytes);
 
 /* Blocking: wait for `stream`, then report whether any finalised factor
- * (R, C or their sum) has been non-finite since create (1) or not (0).
- * Non-finite values are propagated, never masked. */
+ * (R, C or their sum) or any updated vector friction entry has been
+ * non-finite since create (1) or not (0).  Non-finite values are
+ * propagated, never masked. */
 rikfad_status rikfad_nonfinite(rikfad_ctx *ctx, void *stream, int32_t *out);
 
 /* Kernel timing for benchmarks.  While enabled (enable != 0), every step
@@ -241,6 +242,9 @@ rikfad_status ikfad_set_hparams(ikfad_ctx *ctx, const rikfad_hparams *hp);
  * timed steps. */
 rikfad_status ikfad_timing_enable(ikfad_ctx *ctx, int32_t enable);
 rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps);
+/* Blocking: 1 if any updated friction entry has been non-finite since
+ * create, else 0 (as rikfad_nonfinite). */
+rikfad_status ikfad_nonfinite(ikfad_ctx *ctx, void *stream, int32_t *out);
 void ikfad_destroy(ikfad_ctx *ctx);
 
 /* ------------------------------------------------------------------------

@@ -337,7 +337,7 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     if ((s = tm.phase(0, &t0, &t1)) != RIKFAD_OK) return s;
     e = rk::launch_stream(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles, pl.groups.data(),
                           static_cast<int>(pl.groups.size()), ctx->dev.ws, ctx->k,
-                          ctx->pending ? 1 : 0, stream, t0, t1);
+                          ctx->pending ? 1 : 0, ctx->dev.flag, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch stream kernel");
     ctx->pending = false;
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
@@ -535,8 +535,8 @@ rikfad_status ikfad_step(ikfad_ctx *ctx, void *stream_)
     rikfad_status s;
     if ((s = tm.phase(0, &t0, &t1)) != RIKFAD_OK) return s;
     hipError_t e = rk::launch_ikfad(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
-                                    static_cast<int64_t>(ctx->plan.tiles.size()), ctx->k, stream,
-                                    t0, t1);
+                                    static_cast<int64_t>(ctx->plan.tiles.size()), ctx->k,
+                                    ctx->dev.flag, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch ikfad kernel");
     tm.end_step();
     return RIKFAD_OK;
@@ -567,6 +567,16 @@ rikfad_status ikfad_timing_read(ikfad_ctx *ctx, double *ms, int64_t *steps)
     rikfad_status s = read_timing(ctx->timing, t, steps);
     if (s != RIKFAD_OK) return s;
     *ms = t[0];
+    return RIKFAD_OK;
+}
+
+rikfad_status ikfad_nonfinite(ikfad_ctx *ctx, void *stream, int32_t *out)
+{
+    if (!ctx || !out) return fail(RIKFAD_EINVAL, "ctx or out is NULL");
+    HIP_TRY(hipStreamSynchronize(static_cast<hipStream_t>(stream)), "hipStreamSynchronize");
+    int v = 0;
+    HIP_TRY(hipMemcpy(&v, ctx->dev.flag, sizeof(int), hipMemcpyDeviceToHost), "hipMemcpy flag");
+    *out = v ? 1 : 0;
     return RIKFAD_OK;
 }
 

@@ -167,9 +167,11 @@ __device__ void stream_matrix(const TensorDesc &td, const XT *__restrict__ g,
 // Each entry carries its own friction xi: half-kick with xi_n, exact
 // friction update driven by P^(1), half-kick with xi_{n+1}, then D.
 
+// `bad` is set when an updated friction entry is not finite (a non-finite
+// gradient or momentum reaches it in the same step).
 template <int V>
 __device__ __forceinline__ void ikfad_math(float (&xv)[V], const float (&gv)[V], float (&pv)[V],
-                                           float (&fv)[V], const Coeffs &k)
+                                           float (&fv)[V], const Coeffs &k, bool &bad)
 {
 #pragma unroll
     for (int i = 0; i < V; ++i) {
@@ -177,6 +179,7 @@ __device__ __forceinline__ void ikfad_math(float (&xv)[V], const float (&gv)[V],
         xv[i] = xv[i] + k.h * pb;
         const float p1 = pb * exp2f(k.kh * fv[i]);
         fv[i] = k.a * fv[i] + k.kappa * (p1 * p1);
+        bad = bad || !isfinite(fv[i]);
         pv[i] = damp(p1 * exp2f(k.kh * fv[i]), k);
     }
 }
@@ -184,14 +187,14 @@ __device__ __forceinline__ void ikfad_math(float (&xv)[V], const float (&gv)[V],
 template <typename XT, int V>
 __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__restrict__ g,
                                             float *__restrict__ p, float *__restrict__ xi,
-                                            const Coeffs &k)
+                                            const Coeffs &k, bool &bad)
 {
     float xv[V], gv[V], pv[V], fv[V];
     Io<XT, V>::load(x, xv);
     Io<XT, V>::load(g, gv);
     Io<float, V>::load(p, pv);
     Io<float, V>::load(xi, fv);
-    ikfad_math<V>(xv, gv, pv, fv, k);
+    ikfad_math<V>(xv, gv, pv, fv, k, bad);
     Io<XT, V>::store(x, xv);
     Io<float, V>::store(p, pv);
     Io<float, V>::store(xi, fv);
@@ -200,13 +203,15 @@ __device__ __forceinline__ void ikfad_elems(XT *__restrict__ x, const XT *__rest
 // Elements start .. start + count - 1, V per thread access.  With U > 1,
 // batches of U accesses per thread send every load of the batch before its
 // first store (more bytes in flight; costs registers, so only the
-// full-tensor iKFAD kernel's fp32 path uses it).
+// full-tensor iKFAD kernel uses it).  A thread that produced a non-finite
+// friction entry sets *flag.
 template <typename XT, int V, int NTH, int U = 1>
 __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
                                   float *__restrict__ p, float *__restrict__ xi,
-                                  int64_t start, int count, const Coeffs &k)
+                                  int64_t start, int count, const Coeffs &k, int *flag)
 {
     const int full = count - count % V;
+    bool bad = false;
     int e = threadIdx.x * V;
     if (U > 1) {
         for (; e + (U - 1) * NTH * V < full; e += U * NTH * V) {
@@ -222,7 +227,7 @@ __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int64_t o = start + e + u * NTH * V;
-                ikfad_math<V>(xv[u], gv[u], pv[u], fv[u], k);
+                ikfad_math<V>(xv[u], gv[u], pv[u], fv[u], k, bad);
                 Io<XT, V>::store(x + o, xv[u]);
                 Io<float, V>::store(p + o, pv[u]);
                 Io<float, V>::store(xi + o, fv[u]);
@@ -231,26 +236,27 @@ __device__ void elementwise_range(XT *__restrict__ x, const XT *__restrict__ g,
     }
     for (; e < full; e += NTH * V) {
         const int64_t o = start + e;
-        ikfad_elems<XT, V>(x + o, g + o, p + o, xi + o, k);
+        ikfad_elems<XT, V>(x + o, g + o, p + o, xi + o, k, bad);
     }
     for (int e = full + threadIdx.x; e < count; e += NTH) {
         const int64_t o = start + e;
-        ikfad_elems<XT, 1>(x + o, g + o, p + o, xi + o, k);
+        ikfad_elems<XT, 1>(x + o, g + o, p + o, xi + o, k, bad);
     }
+    if (bad) *gmem(flag) = 1;
 }
 
 template <typename XT, int NTH, int U4 = 1>
 __device__ void elementwise_tile(const TensorDesc &td, const void *g, const Tile &tile,
-                                 const Coeffs &k)
+                                 const Coeffs &k, int *flag)
 {
     XT *x = static_cast<XT *>(td.x);
     const XT *gg = static_cast<const XT *>(g);
     if (tile.vec == 8)
-        elementwise_range<XT, 8, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 8, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k, flag);
     else if (tile.vec == 4)
-        elementwise_range<XT, 4, NTH, U4>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 4, NTH, U4>(x, gg, td.p, td.xi, tile.start, tile.count, k, flag);
     else
-        elementwise_range<XT, 1, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k);
+        elementwise_range<XT, 1, NTH>(x, gg, td.p, td.xi, tile.start, tile.count, k, flag);
 }
 
 // ------------------------------------------------------------- kernels
@@ -262,14 +268,14 @@ template <typename XT, int V>
 __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
     const Tile *__restrict__ tiles, int64_t tile0, int64_t ntile, float *__restrict__ ws,
-    Coeffs k, int pending)
+    Coeffs k, int pending, int *__restrict__ flag)
 {
     __shared__ float lds[kStreamWaves * kWave * V];
     const Tile tile = tiles[tile0 + blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
     if (tile.kind == KIND_VECTOR) {
-        elementwise_tile<XT, kStreamThreads>(td, g, tile, k);
+        elementwise_tile<XT, kStreamThreads>(td, g, tile, k, flag);
         return;
     }
     // Tensors whose rows break 16-byte alignment ride along in the same
@@ -441,23 +447,23 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_apply_kernel(
 #endif
 __global__ __launch_bounds__(kThreads) void ikfad_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
-    const Tile *__restrict__ tiles, Coeffs k)
+    const Tile *__restrict__ tiles, Coeffs k, int *__restrict__ flag)
 {
     const Tile tile = tiles[blockIdx.x];
     const TensorDesc td = tensors[tile.tensor];
     const void *g = grads[tile.tensor];
     if (tile.dtype == DT_F32) {
-        elementwise_tile<float, kThreads, kVecIters>(td, g, tile, k);
+        elementwise_tile<float, kThreads, kVecIters>(td, g, tile, k, flag);
     } else if (tile.vec == 8 && RK_IKFAD_BF16_V == 8) {
         elementwise_range<uint16_t, 8, kThreads, RK_IKFAD_BF16_U>(
             static_cast<uint16_t *>(td.x), static_cast<const uint16_t *>(g), td.p, td.xi,
-            tile.start, tile.count, k);
+            tile.start, tile.count, k, flag);
     } else if (tile.vec >= 4) {
         elementwise_range<uint16_t, 4, kThreads, RK_IKFAD_BF16_U>(
             static_cast<uint16_t *>(td.x), static_cast<const uint16_t *>(g), td.p, td.xi,
-            tile.start, tile.count, k);
+            tile.start, tile.count, k, flag);
     } else {
-        elementwise_tile<uint16_t, kThreads>(td, g, tile, k);
+        elementwise_tile<uint16_t, kThreads>(td, g, tile, k, flag);
     }
 }
 
@@ -625,7 +631,8 @@ __global__ __launch_bounds__(kThreads) void probe_read_kernel(const f32x4 *__res
 
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
                          const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
-                         int pending, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                         int pending, int *flag, hipStream_t stream, hipEvent_t start,
+                         hipEvent_t stop)
 {
     const int last = last_group(groups, ngroups);
     for (int q = 0; q < ngroups; ++q) {
@@ -637,14 +644,14 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
         hipError_t e;
         if (gr.dtype == DT_F32)
             e = gr.vec == 4 ? launch(rikfad_stream_kernel<float, 4>, grid, block, stream, a, b,
-                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending)
+                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending, flag)
                             : launch(rikfad_stream_kernel<float, 1>, grid, block, stream, a, b,
-                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending);
+                                     tensors, grads, tiles, gr.begin, gr.count, ws, k, pending, flag);
         else
             e = gr.vec == 4 ? launch(rikfad_stream_kernel<uint16_t, 4>, grid, block, stream, a,
-                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending)
+                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending, flag)
                             : launch(rikfad_stream_kernel<uint16_t, 1>, grid, block, stream, a,
-                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending);
+                                     b, tensors, grads, tiles, gr.begin, gr.count, ws, k, pending, flag);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -685,12 +692,12 @@ hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const Tile
 }
 
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                        int64_t ntiles, const Coeffs &k, hipStream_t stream, hipEvent_t start,
-                        hipEvent_t stop)
+                        int64_t ntiles, const Coeffs &k, int *flag, hipStream_t stream,
+                        hipEvent_t start, hipEvent_t stop)
 {
     if (ntiles <= 0) return hipSuccess;
     return launch(ikfad_kernel, dim3(static_cast<uint32_t>(ntiles)), dim3(kThreads), stream,
-                  start, stop, tensors, grads, tiles, k);
+                  start, stop, tensors, grads, tiles, k, flag);
 }
 
 static uint32_t probe_grid(int64_t units)

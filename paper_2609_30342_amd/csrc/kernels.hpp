@@ -12,10 +12,11 @@ namespace rk {
 
 // Streaming pass over all tiles (matrix and vector) of a context: one
 // launch per tile group.
+// A vector tile whose updated friction is not finite sets *flag.
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
                          const TileGroup *groups, int ngroups, float *ws, const Coeffs &k,
-                         int pending, hipStream_t stream, hipEvent_t start = nullptr,
-                         hipEvent_t stop = nullptr);
+                         int pending, int *flag, hipStream_t stream,
+                         hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 // Finalisation of R, C and the partial sums of R (init_only: sums only),
 // in workgroups of 2^fin_log2 threads (the plan's choice).
@@ -31,7 +32,7 @@ hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const Tile
 
 // Full-tensor element-wise iKFAD.
 hipError_t launch_ikfad(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
-                        int64_t ntiles, const Coeffs &k, hipStream_t stream,
+                        int64_t ntiles, const Coeffs &k, int *flag, hipStream_t stream,
                         hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 hipError_t launch_probe_stream(const float *a, const float *b, const float *c, float *d,

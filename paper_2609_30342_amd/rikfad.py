@@ -93,6 +93,7 @@ _SIGNATURES = {
     "ikfad_set_hparams": (_st, [_vp, _P(rikfad_hparams)]),
     "ikfad_timing_enable": (_st, [_vp, _i32]),
     "ikfad_timing_read": (_st, [_vp, _P(ctypes.c_double), _P(_i64)]),
+    "ikfad_nonfinite": (_st, [_vp, _vp, _P(_i32)]),
     "ikfad_destroy": (None, [_vp]),
     "rikfad_friction_report": (_st, [_vp, _i64, _i64, ctypes.c_double, _i32, _vp,
                                      _P(rikfad_friction_stats)]),
@@ -394,6 +395,26 @@ def _shape2(t):
     return t.shape[0], t.numel() // t.shape[0]
 
 
+def _check_pair(i, x, g):
+    if not (x.is_cuda and g.is_cuda and x.is_contiguous() and g.is_contiguous()):
+        raise ValueError(f"tensor {i}: parameters and gradients must be contiguous "
+                         "device tensors")
+    if g.dtype != x.dtype or g.numel() != x.numel() or g.device != x.device:
+        raise ValueError(f"tensor {i}: gradient does not match its parameter")
+
+
+def _check_state(i, x, tensors, sizes, names):
+    """Caller-provided state: each a contiguous fp32 tensor on x's device with
+    exactly the element count the kernels address (the C ABI sees only
+    pointers, so a short or strided buffer would be read past its end)."""
+    import torch
+    for t, k, nm in zip(tensors, sizes, names):
+        if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or t.device != x.device \
+                or not t.is_contiguous() or t.numel() != k:
+            raise ValueError(f"tensor {i}: state {nm} must be a contiguous fp32 tensor of {k} "
+                             f"elements on {x.device}")
+
+
 class RIKFAD:
     """R-iKFAD over a list of (parameter, gradient) torch tensors on one GPU.
 
@@ -411,14 +432,11 @@ class RIKFAD:
         self.state = []
         structs = []
         for i, (x, g) in enumerate(zip(self.params, self.grads)):
-            if not (x.is_cuda and g.is_cuda and x.is_contiguous() and g.is_contiguous()):
-                raise ValueError(f"tensor {i}: parameters and gradients must be contiguous "
-                                 "device tensors")
-            if g.dtype != x.dtype or g.numel() != x.numel():
-                raise ValueError(f"tensor {i}: gradient does not match its parameter")
+            _check_pair(i, x, g)
             m, n = _shape2(x)
             if state is not None:
                 p, r, c = state[i]
+                _check_state(i, x, (p, r, c), (m * n, m, n), ("p", "r", "c"))
             else:
                 p = torch.zeros((m, n), device=x.device, dtype=torch.float32)
                 r = torch.zeros(m, device=x.device, dtype=torch.float32)
@@ -475,7 +493,8 @@ class IKFAD:
         import torch
         self.params, self.grads, self.state = list(params), list(grads), []
         structs = []
-        for x, g in zip(self.params, self.grads):
+        for i, (x, g) in enumerate(zip(self.params, self.grads)):
+            _check_pair(i, x, g)
             m, n = _shape2(x)
             p = torch.zeros((m, n), device=x.device, dtype=torch.float32)
             xi = torch.zeros((m, n), device=x.device, dtype=torch.float32)
@@ -486,6 +505,12 @@ class IKFAD:
 
     def step(self, stream=None):
         ikfad_step(self.ctx, _stream_handle(stream))
+
+    def nonfinite(self, stream=None):
+        v = ctypes.c_int32()
+        _check(lib().ikfad_nonfinite(self.ctx, _stream_handle(stream), ctypes.byref(v)),
+               "ikfad_nonfinite")
+        return bool(v.value)
 
     def close(self):
         ikfad_destroy(self.ctx)
@@ -513,14 +538,11 @@ class ADAFM:
         self.params, self.grads, self.state = list(params), list(grads), []
         structs = []
         for i, (x, g) in enumerate(zip(self.params, self.grads)):
-            if not (x.is_cuda and g.is_cuda and x.is_contiguous() and g.is_contiguous()):
-                raise ValueError(f"tensor {i}: parameters and gradients must be contiguous "
-                                 "device tensors")
-            if g.dtype != x.dtype or g.numel() != x.numel():
-                raise ValueError(f"tensor {i}: gradient does not match its parameter")
+            _check_pair(i, x, g)
             m, n = _shape2(x)
             if state is not None:
                 mom, r, c = state[i]
+                _check_state(i, x, (mom, r, c), (m * n, m, n), ("first moment", "r", "c"))
             else:
                 mom = torch.zeros((m, n), device=x.device, dtype=torch.float32)
                 r = torch.zeros(m, device=x.device, dtype=torch.float32)

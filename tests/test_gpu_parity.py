@@ -623,6 +623,67 @@ def test_nonfinite_gradient_is_flagged_and_propagated():
         assert torch.isfinite(t).all()
 
 
+def test_nonfinite_vector_gradient_is_flagged():
+    """A NaN in a bias vector's gradient reaches that entry's element-wise
+    friction in the streaming launch, which sets the non-finite flag; the
+    other entries and tensors stay finite."""
+    log("[case] NaN injection into a vector")
+    specs = [S("a", 64, 64), S("v", 1, 300)]
+    pair = make_pair(specs, synth.HP_BASE, seed=9, checked=[])
+    load_grads(pair, 0, 9)
+    pair.opt.step()
+    assert not pair.opt.nonfinite()
+    load_grads(pair, 1, 9)
+    pair.gs[1][0, 17] = float("nan")
+    pair.opt.step()
+    assert pair.opt.nonfinite()
+    _, _, xi = pair.opt.state[1]
+    assert torch.isnan(xi[17]) and torch.isfinite(xi[:17]).all() and torch.isfinite(xi[18:]).all()
+    for t in pair.opt.state[0]:
+        assert torch.isfinite(t).all()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_full_ikfad_flags_nonfinite_friction(dtype):
+    log(f"[case] full iKFAD NaN injection {dtype}")
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = (torch.randn((96, 640), device="cuda") * 0.02).to(dt)
+    g = torch.randn((96, 640), device="cuda").to(dt)
+    ik = R.IKFAD([x], [g], h=0.1, gamma=0.0, alpha=0.1, mu=0.1)
+    ik.step()
+    assert not ik.nonfinite()
+    g[40, 333] = float("inf")
+    ik.step()
+    assert ik.nonfinite()
+    ik.close()
+
+
+def test_binding_rejects_state_it_cannot_address():
+    """The C ABI sees only pointers: the binding refuses caller state that is
+    not a contiguous fp32 buffer of the right size on the parameter's device."""
+    x = torch.zeros((8, 16), device="cuda")
+    g = torch.zeros_like(x)
+    good = (torch.zeros((8, 16), device="cuda"), torch.zeros(8, device="cuda"),
+            torch.zeros(16, device="cuda"))
+    R.RIKFAD([x], [g], h=1e-3, state=[good]).close()
+    bad = [
+        (torch.zeros((8, 15), device="cuda"), good[1], good[2]),              # short p
+        (good[0].double(), good[1], good[2]),                                 # fp64 p
+        (torch.zeros((16, 8), device="cuda").t(), good[1], good[2]),          # strided p
+        (good[0], torch.zeros(7, device="cuda"), good[2]),                    # short r
+        (good[0], good[1], torch.zeros(16)),                                  # host c
+    ]
+    for st in bad:
+        with pytest.raises(ValueError):
+            R.RIKFAD([x], [g], h=1e-3, state=[st])
+        with pytest.raises(ValueError):
+            R.ADAFM([x], [g], h=1e-3, state=[st])
+    with pytest.raises(ValueError):
+        R.IKFAD([x], [g.double()], h=1e-3)
+    with pytest.raises(ValueError):
+        R.IKFAD([torch.zeros((16, 8), device="cuda").t()], [g], h=1e-3)
+
+
 def test_query_reports_state_and_traffic():
     specs = synth.gpt2_small()
     pair = make_pair(specs[:6], synth.HP_BASE, checked=[])
