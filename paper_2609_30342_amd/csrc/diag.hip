@@ -145,9 +145,8 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
     double *__restrict__ rout, double *__restrict__ part, double *__restrict__ spart)
 {
     constexpr bool kWeighted = MODE != kPassSums;
-    constexpr bool kColumns = true;
     constexpr bool kErr = MODE == kPassPowerErr;
-    __shared__ double l[kT / 64][kColumns ? 64 * NC : 1];
+    __shared__ double l[kT / 64][64 * NC];
     __shared__ double ls[kT / 64][2];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const double scale = kWeighted ? inv_norm(vparts, nvparts) : 1.0;
@@ -205,12 +204,9 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
             su = wave_sum(su);
             if (i < r1) {
                 if (MODE == kPassSums && lane == 0) gp(rout)[i] = su;
-                if (kColumns) {
 #pragma unroll
-                    for (int k = 0; k < NC; ++k)
-                        acc[k] += kWeighted ? static_cast<double>(a[k]) * su
-                                            : static_cast<double>(a[k]);
-                }
+                for (int k = 0; k < NC; ++k)
+                    acc[k] += kWeighted ? static_cast<double>(a[k]) * su : static_cast<double>(a[k]);
                 if (kErr) {
 #pragma unroll
                     for (int k = 0; k < NC; ++k) {
@@ -224,10 +220,8 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
             }
         }
     }
-    if (kColumns) {
 #pragma unroll
-        for (int k = 0; k < NC; ++k) l[wave][lane + 64 * k] = acc[k];
-    }
+    for (int k = 0; k < NC; ++k) l[wave][lane + 64 * k] = acc[k];
     if (kErr || MODE == kPassNorm) {
         sa = wave_sum(sa);
         sb = wave_sum(sb);
@@ -237,13 +231,11 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
         }
     }
     __syncthreads();
-    if (kColumns) {
-        for (int64_t j = threadIdx.x; j < n; j += kT) {
-            double s = l[0][j];
+    for (int64_t j = threadIdx.x; j < n; j += kT) {
+        double s = l[0][j];
 #pragma unroll
-            for (int w = 1; w < kT / 64; ++w) s += l[w][j];
-            gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
-        }
+        for (int w = 1; w < kT / 64; ++w) s += l[w][j];
+        gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
     }
     if ((kErr || MODE == kPassNorm) && threadIdx.x == 0) {
         double a = ls[0][0], b = ls[0][1];

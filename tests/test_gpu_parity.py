@@ -22,10 +22,25 @@ S = synth.TensorSpec
 
 
 def test_library_is_the_native_hip_build():
+    """The library these tests call is the in-tree build, mapped into this
+    process, carrying gfx950 code, and its kernels run on the GPU (a probe
+    copies device memory)."""
     import os
-    lib = R.lib()
-    assert os.path.exists(R.LIB_PATH)
-    assert lib is not None
+    R.lib()
+    path = os.path.realpath(R.LIB_PATH)
+    assert os.path.dirname(path) == os.path.realpath(
+        os.path.join(os.path.dirname(__file__), "..", "paper_2609_30342_amd"))
+    with open("/proc/self/maps") as f:
+        assert path in f.read()
+    with open(path, "rb") as f:
+        assert b"gfx950" in f.read()
+    n = 1 << 16
+    a = torch.arange(n, device="cuda", dtype=torch.float32)
+    b = torch.zeros_like(a)
+    R.rikfad_probe_copy(a.data_ptr(), b.data_ptr(), 4 * n,
+                        torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
 
 
 # ------------------------------------------------------------- config 0
