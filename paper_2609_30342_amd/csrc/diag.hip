@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
     // ring is refilled unconditionally (rows past the wave's last are
     // clamped and masked), so every wait is for exactly one row.
     float ring[kPowRing][NC];
-    double rring[kPowRing];
+    double rring[kPowRing] = {};        // row factors (error pass only)
 #pragma unroll
     for (int q = 0; q < kPowRing; ++q) load_row(r0 + q, ring[q], rring[q]);
     double sa = 0.0, sb = 0.0;

@@ -107,6 +107,24 @@ def test_edge_shapes(name, specs):
     assert_ok(errs, label=name)
 
 
+# The read passes' table takes 8 bf16 elements per lane where a matrix's
+# rows allow 16-byte loads, and 4 otherwise, so one set can hold two bf16
+# launches (8-wide with the one-column tiles and vectors, then 4-wide);
+# with x_offset = 4 elements (8 bytes) every bf16 row loses the 16-byte
+# alignment and falls back to 4-wide.
+BF16_WIDTHS = [S("w8", 200, 776, "bf16"), S("w4", 64, 36, "bf16"), S("w1", 65, 27, "bf16"),
+               S("v", 1, 333, "bf16"), S("w8b", 33, 1024, "bf16"), S("f", 70, 96)]
+
+
+@pytest.mark.parametrize("x_offset", [0, 4])
+def test_bf16_read_widths(x_offset):
+    log(f"[case] adafm bf16 read widths x_offset={x_offset} "
+        f"{[(s.m, s.n, s.dtype) for s in BF16_WIDTHS]}")
+    _, errs = run_adafm_parity(BF16_WIDTHS, dict(HP, clip_threshold=0.5), 6, seed=6,
+                               x_offset=x_offset, label=f"bf16 widths off={x_offset}")
+    assert_ok(errs, label="bf16 read widths")
+
+
 def test_misaligned_views_take_scalar_path():
     specs = [S("a", 33, 64), S("b", 1, 50), S("c", 20, 20, "bf16")]
     log("[case] adafm misaligned views")
