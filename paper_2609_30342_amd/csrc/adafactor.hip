@@ -49,6 +49,7 @@ struct Lanes {
     int lane, llog, L, G, seg, nr, nld;
     bool colok;
     int64_t col, lcol, r0;
+    int64_t r_any;     // a row of the tile this wave may read: r0, or the tile's first row
 };
 
 template <int V>
@@ -67,24 +68,89 @@ __device__ __forceinline__ Lanes lanes_of(const Tile &tile)
     t.r0 = tile.start + static_cast<int64_t>(threadIdx.x >> 6) * tile.rpw;
     t.nr = max(0, min(tile.rpw, static_cast<int>(tile.start + tile.count - t.r0)));
     t.nld = (t.nr + t.G - 1) >> (6 - t.llog);
+    t.r_any = t.nr > 0 ? t.r0 : tile.start;
     return t;
 }
 
-// Element offset of row rl of a load; rows outside the wave read its first
-// row (in bounds whenever the wave has rows) and are masked by the caller.
+// Element offset of row rl of a load; rows outside the wave read a row of
+// the tile (its own first row, or the tile's if the wave has none), so the
+// load is always in bounds, and are masked by the caller.
 __device__ __forceinline__ int64_t row_off(const Lanes &t, int rl, int64_t n)
 {
-    return (t.colok && rl < t.nr ? t.r0 + rl : t.r0) * n + t.lcol;
+    return (t.colok && rl < t.nr ? t.r0 + rl : t.r_any) * n + t.lcol;
 }
 
-// Reduces rs over the L lanes of each row of load ld and parks the sum of
-// row ld * G + seg in lane ld * G + seg.
-__device__ __forceinline__ void park_row(float rs, int ld, const Lanes &t, float &myrow)
+// v where keep, else +0, by a bitwise mask: a select on a loaded value can
+// be compiled into a branch around the load, and a load under a branch
+// makes the wave wait for every load it has in flight.
+__device__ __forceinline__ float masked(float v, bool keep)
 {
-    for (int o = 1; o < t.L; o <<= 1) rs += __shfl_xor(rs, o);
-    const int first = ld * t.G;
-    const float v = __shfl(rs, ((t.lane - first) & (t.G - 1)) << t.llog);
-    if (t.lane >= first && t.lane < first + t.G) myrow = v;
+    return __uint_as_float(__float_as_uint(v) & (keep ? 0xffffffffu : 0u));
+}
+
+// Row sums of the statistics pass, kRowChunk row loads at a time.  a[u] is
+// this lane's share of the row of load c0 + u (row (c0 + u) * G + seg); the
+// L lanes of a row are combined pairwise by lane bit 0, 1, 2, ... -- the
+// xor-butterfly tree, so every sum has the same bits as a butterfly per row
+// -- but each exchange hands over half of the loads a lane holds and keeps
+// the other half (lanes with the bit set keep the upper half).  After
+// log2(kRowChunk) exchanges a lane holds one load's sum, which the last
+// exchanges complete; about kRowChunk + log2(L) shuffles per chunk instead
+// of log2(L) + 1 per row, none of them between two row loads.  Lane t then
+// fetches the sum of row t from a lane that holds it.  Chunks of 8 loads
+// (two per 16-row wave) measured faster than 16, which need more registers.
+#ifndef RK_ADA_ROW_CHUNK_LOG2
+#define RK_ADA_ROW_CHUNK_LOG2 3
+#endif
+constexpr int kRowChunkLog2 = RK_ADA_ROW_CHUNK_LOG2;
+constexpr int kRowChunk = 1 << kRowChunkLog2;
+
+__device__ __forceinline__ void park_rows(float (&a)[kRowChunk], int c0, const Lanes &t,
+                                          float &myrow)
+{
+#pragma unroll
+    for (int s = 0; s < kRowChunkLog2; ++s) {
+        const int o = 1 << s;
+        if (o < t.L) {
+            const bool up = (t.lane & o) != 0;
+            constexpr int h0 = kRowChunk >> 1;
+#pragma unroll
+            for (int i = 0; i < (h0 >> s); ++i) {
+                const int h = h0 >> s;
+                // The empty asm keeps the lane-dependent choice a choice of
+                // registers (otherwise it is folded into a choice of address,
+                // which sends a[] to scratch memory).
+                float lo = a[i], hi = a[i + h];
+                asm("" : "+v"(lo), "+v"(hi));
+                const float give = up ? lo : hi;
+                const float keep = up ? hi : lo;
+                a[i] = keep + __shfl_xor(give, o);
+            }
+        }
+    }
+    for (int o = kRowChunk; o < t.L; o <<= 1) a[0] += __shfl_xor(a[0], o);
+    // The halving exchanges done: j = min(log2 L, log2 kRowChunk); a lane
+    // keeps a[0 .. m), m = kRowChunk >> j, the loads whose top j bits
+    // (most significant first) equal its lane bits 0 .. j-1.
+    const int j = t.llog < kRowChunkLog2 ? t.llog : kRowChunkLog2;
+    const int m = kRowChunk >> j;
+    const int rl = t.lane;                       // the row this lane stores
+    const int ld = rl >> (6 - t.llog);
+    const int u = ld - c0;
+    const int seg = rl & (t.G - 1);
+    int sl = 0;
+    for (int b = 0; b < j; ++b) sl |= ((u >> (kRowChunkLog2 - 1 - b)) & 1) << b;
+    const int src = (seg << t.llog) | sl;
+    const int i = u & (m - 1);
+    float v = __shfl(a[0], src);
+#pragma unroll
+    for (int q = 1; q < kRowChunk; ++q) {
+        if (q < m) {
+            const float w = __shfl(a[q], src);
+            if (i == q) v = w;
+        }
+    }
+    if (u >= 0 && u < kRowChunk) myrow = v;
 }
 
 // Workgroup sums of a and b in a fixed order (xor butterfly inside each
@@ -134,6 +200,42 @@ __device__ __forceinline__ float tile_factors(const TensorDesc &td, const Lanes 
     return t.lane < t.nr ? row_factor(gmem(td.r)[t.r0 + t.lane], inv_s) : 0.f;
 }
 
+// The same factors for the read passes, with every load issued at once:
+// columns from the clamped column lcol, the partial sums of R in batches of
+// kChunkLoads per lane (summed in the order of sum_r: lane, lane + 64, ...,
+// then the butterfly), and R from a clamped row.  Identical values.
+constexpr int kChunkLoads = 8;
+
+template <int V>
+__device__ __forceinline__ float read_factors(const TensorDesc &td, const Lanes &t,
+                                              const float *__restrict__ ws, float (&fc)[V])
+{
+    float cv[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) cv[i] = gmem(td.c)[t.lcol + i];
+    const int nch = td.nchunk;
+    const RK_GLOBAL float *part = gmem(ws) + td.chunk;
+    const bool rowok = t.lane < t.nr;
+    const float rv = gmem(td.r)[rowok ? t.r0 + t.lane : t.r_any];
+    float s = 0.f;
+    for (int i0 = 0; i0 < nch; i0 += kWave * kChunkLoads) {
+        float v[kChunkLoads];
+#pragma unroll
+        for (int u = 0; u < kChunkLoads; ++u) {
+            const int idx = i0 + u * kWave + t.lane;
+            v[u] = part[idx < nch ? idx : nch - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < kChunkLoads; ++u) s += masked(v[u], i0 + u * kWave + t.lane < nch);
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) s += __shfl_xor(s, o);
+    const float inv_s = s > 0.f ? 1.f / s : 0.f;
+#pragma unroll
+    for (int i = 0; i < V; ++i) fc[i] = t.colok ? col_factor(cv[i]) : 0.f;
+    return rowok ? row_factor(rv, inv_s) : 0.f;
+}
+
 // Runs op.run<W>(offset) over the elements [start, start + count) of a
 // vector tile, W = the tile's access width, then the scalar tail.
 template <int W, typename Op>
@@ -164,7 +266,10 @@ __device__ void stats_matrix(const TensorDesc &td, const XT *__restrict__ g, con
     // Batches of B row loads, all issued before the first is summed.  The
     // loads are unconditional (rows past the wave's last are clamped into
     // the tensor and masked), so the compiler waits for each row exactly.
+    // The row sums of a chunk of kRowChunk loads are completed together
+    // after its last batch.
     constexpr int B = X2 ? (kReadBatch + 1) / 2 : kReadBatch;
+    static_assert(kRowChunk % B == 0, "whole batches per row chunk");
     const Lanes t = lanes_of<V>(tile);
     const XT *__restrict__ x = static_cast<const XT *>(td.x);
     const int64_t n = td.n;
@@ -172,34 +277,43 @@ __device__ void stats_matrix(const TensorDesc &td, const XT *__restrict__ g, con
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
     float myrow = 0.f;
-    for (int ld0 = 0; ld0 < t.nld; ld0 += B) {
-        typename Raw<XT, V>::type gr[B], xr[B];
+    for (int c0 = 0; c0 < t.nld; c0 += kRowChunk) {
+        float a[kRowChunk];
 #pragma unroll
-        for (int u = 0; u < B; ++u) {
-            const int64_t off = row_off(t, (ld0 + u) * t.G + t.seg, n);
-            gr[u] = Raw<XT, V>::load(g + off);
-            if (X2) xr[u] = Raw<XT, V>::load(x + off);
-        }
+        for (int u = 0; u < kRowChunk; ++u) a[u] = 0.f;
 #pragma unroll
-        for (int u = 0; u < B; ++u) {
-            const bool ok = t.colok && (ld0 + u) * t.G + t.seg < t.nr;
-            float gv[V];
-            Raw<XT, V>::unpack(gr[u], gv);
-            float rs = 0.f;
+        for (int b0 = 0; b0 < kRowChunk; b0 += B) {
+            if (c0 + b0 < t.nld) {
+                typename Raw<XT, V>::type gr[B], xr[B];
 #pragma unroll
-            for (int i = 0; i < V; ++i) {
-                const float q = ok ? gv[i] * gv[i] + k.eps1 : 0.f;
-                acc[i] += q;
-                rs += q;
+                for (int u = 0; u < B; ++u) {
+                    const int64_t off = row_off(t, (c0 + b0 + u) * t.G + t.seg, n);
+                    gr[u] = Raw<XT, V>::load(g + off);
+                    if (X2) xr[u] = Raw<XT, V>::load(x + off);
+                }
+#pragma unroll
+                for (int u = 0; u < B; ++u) {
+                    const bool ok = t.colok && (c0 + b0 + u) * t.G + t.seg < t.nr;
+                    float gv[V];
+                    Raw<XT, V>::unpack(gr[u], gv);
+                    float rs = 0.f;
+#pragma unroll
+                    for (int i = 0; i < V; ++i) {
+                        const float q = ok ? gv[i] * gv[i] + k.eps1 : 0.f;
+                        acc[i] += q;
+                        rs += q;
+                    }
+                    a[b0 + u] = rs;
+                    if (X2) {
+                        float xv[V];
+                        Raw<XT, V>::unpack(xr[u], xv);
+#pragma unroll
+                        for (int i = 0; i < V; ++i) x2 += ok ? xv[i] * xv[i] : 0.f;
+                    }
+                }
             }
-            if (X2) {
-                float xv[V];
-                Raw<XT, V>::unpack(xr[u], xv);
-#pragma unroll
-                for (int i = 0; i < V; ++i) x2 += ok ? xv[i] * xv[i] : 0.f;
-            }
-            park_row(rs, ld0 + u, t, myrow);
         }
+        park_rows(a, c0, t, myrow);
     }
     store_partials<V>(td, tile, ws, acc, myrow, t.nr, t.r0, lds);
 }
@@ -236,8 +350,13 @@ struct StatsVec {
     }
 };
 
+// At least 6 waves per SIMD (three workgroups per CU): the 8-wide bf16
+// instantiation would otherwise take 83 registers and run two workgroups
+// per CU (statistics pass 5.4 against 5.7 TB/s on GPT2-S shapes); the
+// others fit anyway.  The RMS pass runs best as compiled (7 waves).
 template <typename XT, int V, bool X2>
-__global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
+__global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(6)))
+void adafm_stats_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
     const Tile *__restrict__ tiles, int64_t tile0, float *__restrict__ ws,
     float *__restrict__ tilepart, AdaCoeffs k)
@@ -269,20 +388,28 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
 // ---------------------------------------------------------------- pass 2
 
 // Sum of U^2 over one matrix tile (this lane's share), in batches of row
-// loads as in the statistics pass.
+// loads as in the statistics pass.  The first batch goes out before the
+// factor loads, so their round trips overlap.
 template <typename XT, int V>
 __device__ float rms_matrix(const TensorDesc &td, const XT *__restrict__ g, const Tile &tile,
                             const float *__restrict__ ws)
 {
     constexpr int B = kReadBatch;
     const Lanes t = lanes_of<V>(tile);
-    float fc[V];
-    const float myfr = tile_factors<V>(td, t, ws, fc);
+    typename Raw<XT, V>::type gr[B];
     float u2 = 0.f;
-    for (int ld0 = 0; ld0 < t.nld; ld0 += B) {
-        typename Raw<XT, V>::type gr[B];
+    auto issue = [&](int ld0) {
 #pragma unroll
-        for (int u = 0; u < B; ++u) gr[u] = Raw<XT, V>::load(g + row_off(t, (ld0 + u) * t.G + t.seg, td.n));
+        for (int u = 0; u < B; ++u)
+            gr[u] = Raw<XT, V>::load(g + row_off(t, (ld0 + u) * t.G + t.seg, td.n));
+    };
+    issue(0);
+    float fc[V];
+    const float myfr = read_factors<V>(td, t, ws, fc);
+    auto sum = [&](int ld0) {
+        // u2 + uu * uu stays a product and a sum (never fused), in every
+        // row alike, so the sum does not depend on code placement.
+#pragma clang fp contract(off)
 #pragma unroll
         for (int u = 0; u < B; ++u) {
             const int rl = (ld0 + u) * t.G + t.seg;
@@ -296,6 +423,11 @@ __device__ float rms_matrix(const TensorDesc &td, const XT *__restrict__ g, cons
                 u2 += ok ? uu * uu : 0.f;
             }
         }
+    };
+    sum(0);
+    for (int ld0 = B; ld0 < t.nld; ld0 += B) {
+        issue(ld0);
+        sum(ld0);
     }
     return u2;
 }
