@@ -326,7 +326,7 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     if (pl.tiles.empty()) return RIKFAD_OK;
     hipError_t e;
     if (!ctx->sums_valid && pl.row_items > 0) {
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, pl.row_items, pl.fin_log2,
+        e = rk::launch_finalize(ctx->dev.fin, pl.row_items, pl.fin_log2,
                                 ctx->dev.ws, ctx->k, ctx->dev.flag, 1, stream);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel (init)");
     }
@@ -343,7 +343,7 @@ rikfad_status rikfad_step(rikfad_ctx *ctx, void *stream_)
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
     t0 = t1 = nullptr;
     if (nfin > 0 && (s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
-    e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
+    e = rk::launch_finalize(ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
                             ctx->k, ctx->dev.flag, 0, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
     ctx->pending = pl.matrix_tiles > 0;
@@ -758,7 +758,7 @@ rikfad_status adafm_step(adafm_ctx *ctx, void *stream_)
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
     if (nfin > 0) {
         if ((s = tm.phase(1, &t0, &t1)) != RIKFAD_OK) return s;
-        e = rk::launch_finalize(ctx->dev.tensors, ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
+        e = rk::launch_finalize(ctx->dev.fin, nfin, pl.fin_log2, ctx->dev.ws,
                                 fk, ctx->dev.flag, 0, stream, t0, t1);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
     }

@@ -236,7 +236,7 @@ __device__ __forceinline__ float damp(float v, const Coeffs &k)
 // walked its rows.  acc[V]: this lane's column sums; myrow: in lane t, the
 // sum of the wave's row r0 + t (t < nr).  Lanes l and l ^ o (o >= L) own the
 // same columns and are folded first, then the waves through LDS in wave
-// order; the tile writes its column partials (row `stripe` of colpart) and
+// order; the tile writes its column partials (stripe `stripe` of colpart) and
 // each wave its row partials (row `cb` of rowpart).  Every thread of the
 // workgroup must call this (it synchronises the workgroup).
 template <int V>
@@ -257,14 +257,14 @@ __device__ __forceinline__ void store_partials(const TensorDesc &td, const Tile 
         for (int i = 0; i < V; ++i) lds[wave * kWave * V + ccol + i] = acc[i];
     }
     __syncthreads();
-    float *colpart = ws + td.colpart + static_cast<int64_t>(tile.stripe) * td.n + tile.col0;
+    float *colpart = ws + td.colpart;
     for (int j = threadIdx.x; j < tile.ncols; j += kStreamWaves * kWave) {
         float sum = lds[j];
 #pragma unroll
         for (int w = 1; w < kStreamWaves; ++w) sum += lds[w * kWave * V + j];
-        gmem(colpart)[j] = sum;
+        gmem(colpart)[colpart_index(tile.col0 + j, tile.stripe, td.nrs)] = sum;
     }
-    if (lane < nr) gmem(ws)[td.rowpart + static_cast<int64_t>(tile.cb) * td.m + r0 + lane] = myrow;
+    if (lane < nr) gmem(ws)[td.rowpart + static_cast<int64_t>(tile.cb) * pad4(td.m) + r0 + lane] = myrow;
 }
 
 }  // namespace rk

@@ -286,97 +286,139 @@ __global__ __launch_bounds__(kStreamThreads) void rikfad_stream_kernel(
         stream_matrix<XT, V>(td, static_cast<const XT *>(g), tile, ws, k, pending, lds);
 }
 
-// Finalisation (C.2 / C.3 stage 2), one launch.  Row items: thread t owns
-// row start+t, sums its column-block partials in block order, updates R,
-// and the workgroup writes the fixed-order sum of each 256 new R values.
-// Column items: thread (q, c) of S stripe lanes x W = 256 / S columns sums
-// the stripes q, q + S, q + 2S, ... of column start+c in that order
-// (kColLoads loads in flight), and the S lane sums of a column are folded
-// pairwise through LDS (lane q takes lane q + h for h = S/2, ..., 1): a
-// fixed tree, so the result does not depend on timing.  init_only
-// recomputes the partial sums of R from R as it stands.
+// Finalisation (C.2 / C.3 stage 2), one launch of T-thread workgroups.
+// Every thread handles 4 rows or 4 columns and reads their partial sums 16
+// bytes at a time.  Row items: thread t owns rows start + 4t .. + 3, sums
+// their column-block partials in block order and updates R; the 256 rows of
+// a wave give one partial sum of R (each thread's four new values in order,
+// then a butterfly across the wave).  Column items: thread t owns columns
+// 4(t mod 4) .. + 3 of a 16-column group and stripe lane q of S; it sums
+// stripes q, q + S, q + 2S, ... in that order (kFinLoads loads in flight;
+// the lanes of a wave read consecutive stripes of a group, one contiguous
+// run), the stripe lanes of a wave fold by a butterfly and, past 16 lanes,
+// the waves of a group fold in order through LDS.  Every sum has a fixed
+// order, so the result does not depend on timing.  init_only recomputes the
+// partial sums of R from R as it stands (row items only).
 template <int LOG2T>
 __global__ __launch_bounds__(1 << LOG2T) void rikfad_finalize_kernel(
-    const TensorDesc *__restrict__ tensors, const FinItem *__restrict__ items,
-    float *__restrict__ ws, Coeffs k, int *__restrict__ flag, int init_only)
+    const FinItem *__restrict__ items, float *__restrict__ ws, Coeffs k, int *__restrict__ flag,
+    int init_only)
 {
     constexpr int T = 1 << LOG2T;
-    static_assert(T % kChunkRows == 0 && kChunkRows == 4 * kWave,
-                  "row items cover whole 256-row chunks, four waves each");
-    __shared__ float lds[T];
+    static_assert(kChunkRows == 4 * kWave, "a wave of row items covers one 256-row chunk");
+    __shared__ f32x4 lds[T / kWave * 4];
     const FinItem it = items[blockIdx.x];
-    const TensorDesc td = tensors[it.tensor];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x >> 6;
+    bool bad = false;
     if (it.kind == FIN_ROWS) {
-        const int t = threadIdx.x;
-        float rv = 0.f;
-        if (t < it.count) {
-            const int64_t i = static_cast<int64_t>(it.start) + t;
-            rv = gmem(td.r)[i];
+        const int t0 = 4 * static_cast<int>(threadIdx.x);
+        float rv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (t0 < it.count) {
+            const int nv = min(4, it.count - t0);
+            const int64_t i0 = static_cast<int64_t>(it.start) + t0;
+            // R first and unconditionally (rows clamped into the tensor),
+            // so its loads travel with the partial sums' instead of after.
+            float r[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) r[j] = gmem(it.f)[min(i0 + j, it.len - 1)];
+            f32x4 s = {0.f, 0.f, 0.f, 0.f};
             if (!init_only) {
-                const RK_GLOBAL float *rp = gmem(ws) + td.rowpart + i;
-                float s = 0.f;
-                for (int cb = 0; cb < td.ncb; cb += 16) {
-                    float v[16];
+                const int64_t stride = pad4(it.len) >> 2;
+                const RK_GLOBAL f32x4 *rp =
+                    reinterpret_cast<const RK_GLOBAL f32x4 *>(gmem(ws) + it.part + i0);
+                for (int cb = 0; cb < it.nparts; cb += kFinRowLoads) {
+                    // Unconditional loads (clamped to the last block, the
+                    // value masked) keep every load of the batch in flight.
+                    f32x4 v[kFinRowLoads];
 #pragma unroll
-                    for (int q = 0; q < 16; ++q)
-                        v[q] = cb + q < td.ncb ? rp[static_cast<int64_t>(cb + q) * td.m] : 0.f;
+                    for (int u = 0; u < kFinRowLoads; ++u) {
+                        const f32x4 w = rp[static_cast<int64_t>(min(cb + u, it.nparts - 1)) * stride];
+                        v[u] = cb + u < it.nparts ? w : f32x4{0.f, 0.f, 0.f, 0.f};
+                    }
 #pragma unroll
-                    for (int q = 0; q < 16; ++q) s += v[q];
+                    for (int u = 0; u < kFinRowLoads; ++u) s += v[u];
                 }
-                rv = k.a * rv + k.kappa * s;
-                gmem(td.r)[i] = rv;
             }
-            if (!isfinite(rv)) *gmem(flag) = 1;
+            const float sv[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float rn = init_only ? r[j] : k.a * r[j] + k.kappa * sv[j];
+                if (j < nv) {
+                    if (!init_only) gmem(it.f)[i0 + j] = rn;
+                    rv[j] = rn;
+                    bad = bad || !isfinite(rn);
+                }
+            }
         }
-        // One partial sum of R per 256 rows (four waves, folded in order).
-        float v = rv;
+        float v = ((rv[0] + rv[1]) + rv[2]) + rv[3];
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o);
-        if ((threadIdx.x & (kWave - 1)) == 0) lds[threadIdx.x >> 6] = v;
-        __syncthreads();
-        const int q = threadIdx.x;
-        if (q < T / kChunkRows && q * kChunkRows < it.count) {
-            const float *l = lds + 4 * q;
-            const float s = ((l[0] + l[1]) + l[2]) + l[3];
-            gmem(ws)[td.chunk + it.chunk + q] = s;
-            if (!isfinite(s)) *gmem(flag) = 1;
+        if (lane == 0 && wave * kChunkRows < it.count) {
+            gmem(ws)[it.chunk + wave] = v;
+            bad = bad || !isfinite(v);
         }
     } else {
         const int slog = it.lanes_log2;
-        const int S = 1 << slog;
-        const int W = T >> slog;
-        const int c = threadIdx.x & (W - 1);
-        const int q = threadIdx.x >> (LOG2T - slog);
-        float s = 0.f;
-        if (c < it.count) {
-            const RK_GLOBAL float *cp = gmem(ws) + td.colpart + it.start + c;
-            for (int s0 = q; s0 < td.nrs; s0 += S * kColLoads) {
-                float v[kColLoads];
+        const int S = 1 << slog;                   // stripe lanes
+        const int c4 = threadIdx.x & 3;
+        const int q = (threadIdx.x >> 2) & (S - 1);
+        const int g = threadIdx.x >> (2 + slog);   // group of 16 columns
+        const int c0 = 16 * g + 4 * c4;            // first column, from start
+        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+        float cv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (c0 < it.count) {
+            const int64_t j0 = static_cast<int64_t>(it.start) + c0;
+            // C first and unconditionally (columns clamped into the tensor).
+            if (q == 0) {
 #pragma unroll
-                for (int u = 0; u < kColLoads; ++u) {
+                for (int j = 0; j < 4; ++j) cv[j] = gmem(it.f)[min(j0 + j, it.len - 1)];
+            }
+            const RK_GLOBAL f32x4 *cp = reinterpret_cast<const RK_GLOBAL f32x4 *>(
+                gmem(ws) + it.part + colpart_index(j0, 0, it.nparts));
+            for (int s0 = q; s0 < it.nparts; s0 += S * kFinLoads) {
+                f32x4 v[kFinLoads];
+#pragma unroll
+                for (int u = 0; u < kFinLoads; ++u) {
                     const int st = s0 + u * S;
-                    v[u] = st < td.nrs ? cp[static_cast<int64_t>(st) * td.n] : 0.f;
+                    const f32x4 w = cp[static_cast<int64_t>(min(st, it.nparts - 1)) * (kColGroup / 4)];
+                    v[u] = st < it.nparts ? w : f32x4{0.f, 0.f, 0.f, 0.f};
                 }
 #pragma unroll
-                for (int u = 0; u < kColLoads; ++u) s += v[u];
+                for (int u = 0; u < kFinLoads; ++u) s += v[u];
             }
         }
-        if (slog > 0) {
-            lds[threadIdx.x] = s;
-            for (int h = S >> 1; h > 0; h >>= 1) {
-                __syncthreads();
-                if (q < h) lds[threadIdx.x] += lds[threadIdx.x + h * W];
-            }
+        // Stripe lanes of one wave that share columns: lanes l and l ^ o,
+        // o = 4, 8, ... below 4S (at most 16 lanes of a wave).
+        for (int o = 4; o < min(4 * S, kWave); o <<= 1) {
+            s.x += __shfl_xor(s.x, o);
+            s.y += __shfl_xor(s.y, o);
+            s.z += __shfl_xor(s.z, o);
+            s.w += __shfl_xor(s.w, o);
+        }
+        // More than 16 stripe lanes: the S / 16 waves of a group, in order.
+        if (S > kWave / 4) {
+            const int wpg = S / (kWave / 4);
+            if (lane < 4) lds[wave * 4 + c4] = s;
             __syncthreads();
-            s = lds[c];
+            if (q == 0) {
+                s = lds[wave * 4 + c4];
+                for (int w = 1; w < wpg; ++w) s += lds[(wave + w) * 4 + c4];
+            }
         }
-        if (q == 0 && c < it.count) {
-            const int64_t jj = static_cast<int64_t>(it.start) + c;
-            const float cvn = k.a * gmem(td.c)[jj] + k.kappa * s;
-            gmem(td.c)[jj] = cvn;
-            if (!isfinite(cvn)) *gmem(flag) = 1;
+        if (q == 0 && c0 < it.count) {
+            const float sv[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float cvn = k.a * cv[j] + k.kappa * sv[j];
+                if (c0 + j < it.count) {
+                    gmem(it.f)[static_cast<int64_t>(it.start) + c0 + j] = cvn;
+                    bad = bad || !isfinite(cvn);
+                }
+            }
         }
     }
+    if (bad) *gmem(flag) = 1;
 }
 
 // Second half-kick + D on stored P^(1): p <- d (p .* exp(-(h/2) xi~)) with
@@ -657,17 +699,17 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
     return hipSuccess;
 }
 
-hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
-                           int fin_log2, float *ws, const Coeffs &k, int *flag, int init_only,
-                           hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+hipError_t launch_finalize(const FinItem *items, int64_t nitems, int fin_log2, float *ws,
+                           const Coeffs &k, int *flag, int init_only, hipStream_t stream,
+                           hipEvent_t start, hipEvent_t stop)
 {
     if (nitems <= 0) return hipSuccess;
     const dim3 grid(static_cast<uint32_t>(nitems));
     if (fin_log2 == kFinLargeLog2)
         return launch(rikfad_finalize_kernel<kFinLargeLog2>, grid, dim3(1 << kFinLargeLog2),
-                      stream, start, stop, tensors, items, ws, k, flag, init_only);
+                      stream, start, stop, items, ws, k, flag, init_only);
     return launch(rikfad_finalize_kernel<kFinSmallLog2>, grid, dim3(1 << kFinSmallLog2), stream,
-                  start, stop, tensors, items, ws, k, flag, init_only);
+                  start, stop, items, ws, k, flag, init_only);
 }
 
 hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,

@@ -20,10 +20,9 @@ hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, co
 
 // Finalisation of R, C and the partial sums of R (init_only: sums only),
 // in workgroups of 2^fin_log2 threads (the plan's choice).
-hipError_t launch_finalize(const TensorDesc *tensors, const FinItem *items, int64_t nitems,
-                           int fin_log2, float *ws, const Coeffs &k, int *flag, int init_only,
-                           hipStream_t stream, hipEvent_t start = nullptr,
-                           hipEvent_t stop = nullptr);
+hipError_t launch_finalize(const FinItem *items, int64_t nitems, int fin_log2, float *ws,
+                           const Coeffs &k, int *flag, int init_only, hipStream_t stream,
+                           hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 // Second half-kick + D over the matrix tiles of every tile group.
 hipError_t launch_apply(const TensorDesc *tensors, const Tile *tiles, const TileGroup *groups,

@@ -36,7 +36,7 @@ constexpr int kRingBF16 = RK_RING_BF16;         // the same for bf16 x/g
 constexpr int kMaxRowsPerWave = 64;             // lane t keeps row t's partial sum
 constexpr int kBlockLanes = RK_BLOCK_LANES;     // lanes per row of a full column block
 constexpr int kRowsPerWave = RK_ROWS_PER_WAVE;  // rows per wave of a matrix tile
-constexpr int kChunkRows = kThreads;            // rows per finalisation item
+constexpr int kChunkRows = kThreads;            // rows per partial sum of R
 constexpr int kSmallSetTiles = 256;             // compute units of the chip
 constexpr int kVecIters = 4;                    // vector tile = kThreads*vec*kVecIters
 static_assert(kStreamWaves >= 1 && kStreamWaves <= 16, "a workgroup holds at most 16 waves");
@@ -51,11 +51,37 @@ enum : int32_t { FIN_ROWS = 0, FIN_COLS = 1 };
 
 // Finalisation workgroups: 256 threads, or 1024 for sets with a matrix of
 // more than 512 row stripes (about 16K rows), whose column items need more
-// stripe lanes than 256 threads hold at 16 columns each.
+// stripe lanes than 256 threads hold at 16 columns each.  Every thread of
+// the finalisation handles 4 rows or 4 columns with 16-byte accesses to the
+// partial sums.
+#ifndef RK_FIN_LARGE_LOG2
+#define RK_FIN_LARGE_LOG2 10
+#endif
 constexpr int kFinSmallLog2 = 8;
-constexpr int kFinLargeLog2 = 10;
-constexpr int kColLoads = 32;                   // column partials in flight per thread
-constexpr int kMinColsLog2 = 4;                 // at least 16 columns (64 bytes) per column item
+constexpr int kFinLargeLog2 = RK_FIN_LARGE_LOG2;
+#ifndef RK_FIN_LOADS
+#define RK_FIN_LOADS 8
+#endif
+#ifndef RK_FIN_ROW_LOADS
+#define RK_FIN_ROW_LOADS 4
+#endif
+constexpr int kFinLoads = RK_FIN_LOADS;         // 16-byte column partial loads in flight per thread
+constexpr int kFinRowLoads = RK_FIN_ROW_LOADS;  // the same for row partials (row items)
+static_assert(kFinLargeLog2 >= kFinSmallLog2 && kFinLargeLog2 <= 10, "finalisation workgroup");
+
+// Row partials are [ncb][pad4(m)]: each block's row sums padded to a
+// multiple of 4 floats, so that the finalisation reads 4 rows' partial sums
+// with one 16-byte access (the padding is never written or used).  Column
+// partials are kept in groups of 16 columns, each group holding all of its
+// stripes one after the other ([ceil(n/16)][nrs][16], 64-byte rows): a
+// finalisation item then reads each group's stripes as one contiguous run.
+constexpr int64_t pad4(int64_t v) { return (v + 3) & ~int64_t(3); }
+constexpr int kColGroup = 16;
+constexpr int64_t colpart_index(int64_t j, int64_t stripe, int64_t nrs)
+{
+    return (j >> 4) * (nrs << 4) + (stripe << 4) + (j & 15);
+}
+constexpr int64_t colpart_floats(int64_t n, int64_t nrs) { return ((n + 15) >> 4) * (nrs << 4); }
 
 // One parameter tensor.  Offsets are in floats into the context workspace.
 struct TensorDesc {
@@ -65,8 +91,8 @@ struct TensorDesc {
     float *c;          // n column factor (matrix)
     float *xi;         // m*n element-wise friction (vector / full iKFAD)
     int64_t m, n;
-    int64_t rowpart;   // [ncb][m] row partial sums of [P^(1)]^2
-    int64_t colpart;   // [nrs][n] column partial sums of [P^(1)]^2
+    int64_t rowpart;   // [ncb][pad4(m)] row partial sums of [P^(1)]^2
+    int64_t colpart;   // [ceil(n/16)][nrs][16] column partial sums of [P^(1)]^2
     int64_t chunk;     // [nchunk] partial sums of R
     int32_t nchunk, ncb, nrs, dtype;
     int32_t kind, vec;
@@ -103,19 +129,27 @@ struct TileGroup {
     int64_t count;
 };
 
-// One workgroup of the finalisation pass (one launch).
-//   FIN_ROWS  T rows (T = threads of the workgroup): R update and one
-//             partial sum of R per 256 rows.
-//   FIN_COLS  T / S columns, all row stripes: C update.  The T threads are
-//             S = 2^lanes_log2 stripe lanes x T / S columns, S the smallest
-//             power of two that leaves each thread at most kColLoads
-//             stripes, capped so that an item keeps at least 16 columns.
+// One workgroup of the finalisation pass (one launch), T threads.
+//   FIN_ROWS  4T rows, 4 per thread: R update and one partial sum of R per
+//             256 rows (one wave).  start is a multiple of 4T.
+//   FIN_COLS  4T / S columns, all row stripes: C update.  Thread t takes
+//             columns 4(t mod 4) .. +3 of group t / 4S (16 columns each)
+//             and stripe lane (t / 4) mod S, S = 2^lanes_log2 the smallest
+//             power of two that leaves each thread at most kFinLoads
+//             stripes, capped so that an item keeps at least one group.
+//             start is a multiple of 16.
+// An item carries what it needs of its tensor, so that a workgroup's first
+// load is its only descriptor load.
 struct FinItem {
+    float *f;          // R (FIN_ROWS) or C (FIN_COLS) of the tensor
+    int64_t len;       // m (FIN_ROWS) or n (FIN_COLS)
+    int64_t part;      // workspace offset of the tensor's row / column partials
+    int64_t chunk;     // FIN_ROWS: workspace offset of the first partial sum of R it writes
     int32_t tensor;
     int32_t kind;
     int32_t start;     // first row / column
     int32_t count;     // rows / columns
-    int32_t chunk;     // FIN_ROWS: the partial sum of R it writes
+    int32_t nparts;    // FIN_ROWS: column blocks (ncb); FIN_COLS: row stripes (nrs)
     int32_t lanes_log2;// FIN_COLS: log2 of the stripe lanes S
 };
 

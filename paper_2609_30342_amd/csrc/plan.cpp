@@ -267,9 +267,9 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         d.nrs = static_cast<int32_t>(ceil_div(T.m, stripe_rows));
         d.nchunk = static_cast<int32_t>(ceil_div(T.m, kChunkRows));
         d.rowpart = ws;
-        ws += round_up(T.m * d.ncb, 64);
+        ws += round_up(pad4(T.m) * d.ncb, 64);
         d.colpart = ws;
-        ws += round_up(int64_t(d.nrs) * T.n, 64);
+        ws += round_up(colpart_floats(T.n, d.nrs), 64);
         d.chunk = ws;
         ws += round_up(d.nchunk, 64);
 
@@ -312,27 +312,32 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
             mat_tiles[cls].push_back(tl);
         }
     }
-    // Finalisation items (layout.hpp), sized for the set's workgroup.
+    // Finalisation items (layout.hpp), sized for the set's workgroup: 1024
+    // threads when some matrix has more stripes than 256 threads cover at
+    // 16 columns per item and kFinLoads stripes per thread.
     for (const TensorDesc &d : pl.tensors)
-        if (d.kind == KIND_MATRIX && d.nrs > (int64_t(kColLoads) << (kFinSmallLog2 - kMinColsLog2)))
+        if (d.kind == KIND_MATRIX && d.nrs > (int64_t(kFinLoads) << (kFinSmallLog2 - 2)))
             pl.fin_log2 = kFinLargeLog2;
     const int64_t fin_threads = int64_t(1) << pl.fin_log2;
-    const int max_slog = pl.fin_log2 - kMinColsLog2;
+    const int max_slog = pl.fin_log2 - 2;
     for (int64_t i = 0; i < count; ++i) {
         const TensorDesc &d = pl.tensors[static_cast<size_t>(i)];
         if (d.kind != KIND_MATRIX) continue;
-        // Row items: one row per thread, one partial sum of R per 256 rows.
-        for (int64_t r0 = 0; r0 < d.m; r0 += fin_threads)
-            pl.fin.push_back({static_cast<int32_t>(i), FIN_ROWS, static_cast<int32_t>(r0),
-                              static_cast<int32_t>(d.m - r0 < fin_threads ? d.m - r0 : fin_threads),
-                              static_cast<int32_t>(r0 / kChunkRows), 0});
-        // Column items: S stripe lanes x fin_threads / S columns.
+        // Row items: 4 rows per thread, one partial sum of R per 256 rows.
+        const int64_t rows = 4 * fin_threads;
+        for (int64_t r0 = 0; r0 < d.m; r0 += rows)
+            pl.fin.push_back({d.r, d.m, d.rowpart, d.chunk + r0 / kChunkRows,
+                              static_cast<int32_t>(i), FIN_ROWS, static_cast<int32_t>(r0),
+                              static_cast<int32_t>(d.m - r0 < rows ? d.m - r0 : rows), d.ncb, 0});
+        // Column items: S stripe lanes x fin_threads / S threads of 4 columns.
         int slog = 0;
-        while (slog < max_slog && (int64_t(kColLoads) << slog) < d.nrs) ++slog;
-        const int64_t W = fin_threads >> slog;
-        for (int64_t j0 = 0; j0 < d.n; j0 += W)
-            col_items.push_back({static_cast<int32_t>(i), FIN_COLS, static_cast<int32_t>(j0),
-                                 static_cast<int32_t>(d.n - j0 < W ? d.n - j0 : W), 0, slog});
+        while (slog < max_slog && (int64_t(kFinLoads) << slog) < d.nrs) ++slog;
+        const int64_t cols = 4 * (fin_threads >> slog);
+        for (int64_t j0 = 0; j0 < d.n; j0 += cols)
+            col_items.push_back({d.c, d.n, d.colpart, 0, static_cast<int32_t>(i), FIN_COLS,
+                                 static_cast<int32_t>(j0),
+                                 static_cast<int32_t>(d.n - j0 < cols ? d.n - j0 : cols), d.nrs,
+                                 slog});
     }
     // One launch per storage type: its widest matrix tiles, then its
     // one-column matrix tiles (served by the same launch), then its vector

@@ -48,6 +48,14 @@ struct Marks {
             if (!b) return false;
         return true;
     }
+    // every entry of rows of `stride` entries whose column is below `used`
+    // (the padding at the end of each row is never written)
+    bool all_rows(int64_t stride, int64_t used) const
+    {
+        for (size_t i = 0; i < v.size(); ++i)
+            if (static_cast<int64_t>(i) % stride < used && !v[i]) return false;
+        return true;
+    }
 };
 
 static int ring_depth(int32_t dtype) { return dtype == DT_F32 ? kRingF32 : kRingBF16; }
@@ -96,11 +104,13 @@ static void check_matrix_tile(const Plan &pl, const Tile &tl, std::vector<Marks>
                 }
             }
             if (lane < nr)
-                rowp[static_cast<size_t>(tl.tensor)].hit(int64_t(tl.cb) * m + r0 + lane, "rowpart");
+                rowp[static_cast<size_t>(tl.tensor)].hit(int64_t(tl.cb) * pad4(m) + r0 + lane,
+                                                         "rowpart");
         }
     }
     for (int j = 0; j < tl.ncols; ++j)
-        colp[static_cast<size_t>(tl.tensor)].hit(int64_t(tl.stripe) * n + tl.col0 + j, "colpart");
+        colp[static_cast<size_t>(tl.tensor)].hit(colpart_index(tl.col0 + j, tl.stripe, td.nrs),
+                                                 "colpart");
 }
 
 static void check_vector_tile(const Plan &pl, const Tile &tl, std::vector<Marks> &elems)
@@ -115,10 +125,10 @@ static void check_vector_tile(const Plan &pl, const Tile &tl, std::vector<Marks>
 static void check_plan(const Plan &pl, int64_t count)
 {
     // 1024-thread finalisation exactly when some matrix has more row
-    // stripes than 16 stripe lanes of 32 loads cover
+    // stripes than 64 stripe lanes of kFinLoads loads cover
     bool tall = false;
     for (const TensorDesc &td : pl.tensors)
-        tall = tall || (td.kind == KIND_MATRIX && td.nrs > kColLoads * 16);
+        tall = tall || (td.kind == KIND_MATRIX && td.nrs > kFinLoads * 64);
     CHECK(pl.fin_log2 == (tall ? kFinLargeLog2 : kFinSmallLog2), "finalisation workgroup size");
     std::vector<Marks> elems(static_cast<size_t>(count)), rowp(static_cast<size_t>(count)),
         colp(static_cast<size_t>(count)), chunks(static_cast<size_t>(count)),
@@ -129,13 +139,14 @@ static void check_plan(const Plan &pl, int64_t count)
         const TensorDesc &td = pl.tensors[static_cast<size_t>(i)];
         elems[static_cast<size_t>(i)].init(td.m * td.n);
         if (td.kind == KIND_MATRIX) {
-            rowp[static_cast<size_t>(i)].init(int64_t(td.ncb) * td.m);
-            colp[static_cast<size_t>(i)].init(int64_t(td.nrs) * td.n);
+            rowp[static_cast<size_t>(i)].init(int64_t(td.ncb) * pad4(td.m));
+            colp[static_cast<size_t>(i)].init(colpart_floats(td.n, td.nrs));
             chunks[static_cast<size_t>(i)].init(td.nchunk);
             cols[static_cast<size_t>(i)].init(td.n);
             rows[static_cast<size_t>(i)].init(td.m);
-            regions.push_back({td.rowpart, int64_t(td.ncb) * td.m});
-            regions.push_back({td.colpart, int64_t(td.nrs) * td.n});
+            CHECK(td.rowpart % 4 == 0 && td.colpart % 4 == 0, "partials not 16-byte aligned");
+            regions.push_back({td.rowpart, int64_t(td.ncb) * pad4(td.m)});
+            regions.push_back({td.colpart, colpart_floats(td.n, td.nrs)});
             regions.push_back({td.chunk, td.nchunk});
         }
     }
@@ -180,7 +191,9 @@ static void check_plan(const Plan &pl, int64_t count)
         if (tl.kind == KIND_MATRIX) check_matrix_tile(pl, tl, elems, rowp, colp);
         else check_vector_tile(pl, tl, elems);
     }
-    // finalisation items
+    // finalisation items: replays rikfad_finalize_kernel's indexing (4 rows
+    // or 4 columns per thread, 16-byte partial-sum reads)
+    const int T = 1 << pl.fin_log2;
     const int64_t nfin = static_cast<int64_t>(pl.fin.size());
     for (int64_t q = 0; q < nfin; ++q) {
         const FinItem &it = pl.fin[static_cast<size_t>(q)];
@@ -188,52 +201,87 @@ static void check_plan(const Plan &pl, int64_t count)
         CHECK(td.kind == KIND_MATRIX, "finalisation item on a vector");
         if (it.kind == FIN_ROWS) {
             CHECK(q < pl.row_items, "row item after the row range");
-            CHECK(it.count >= 1 && it.count <= (1 << pl.fin_log2), "row item count");
-            CHECK(it.start % kChunkRows == 0 && it.chunk == it.start / kChunkRows,
-                  "row item chunk alignment");
-            for (int t = 0; t < it.count; ++t) {
-                rows[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + t, "row item row");
-                for (int cb = 0; cb < td.ncb; ++cb)
-                    CHECK(int64_t(cb) * td.m + it.start + t < int64_t(td.ncb) * td.m, "rowpart read");
-            }
-            // the kernel writes chunk sums for q < kFinThreads / 256 while
-            // q * 256 < count
-            for (int q = 0; q < (1 << pl.fin_log2) / kChunkRows && q * kChunkRows < it.count; ++q)
-                chunks[static_cast<size_t>(it.tensor)].hit(it.chunk + q, "chunk");
-        } else {
-            // Replays the column item: thread (q, c), S stripe lanes x W
-            // columns; every stripe of every column read once, each column
-            // updated once, and stripe lanes enough for at most kColLoads
-            // stripes per thread unless that would leave fewer than 16
-            // columns.
-            CHECK(it.kind == FIN_COLS && q >= pl.row_items, "column item placement");
-            const int slog = it.lanes_log2, max_slog = pl.fin_log2 - kMinColsLog2;
-            CHECK(slog >= 0 && slog <= max_slog, "stripe lanes log2 %d", slog);
-            const int S = 1 << slog, W = (1 << pl.fin_log2) >> slog;
-            CHECK(it.count >= 1 && it.count <= W, "column item count %d W %d", it.count, W);
-            CHECK((int64_t(kColLoads) << slog) >= td.nrs || slog == max_slog,
-                  "stripe lanes too few for %d stripes", td.nrs);
-            CHECK(slog == 0 || (int64_t(kColLoads) << (slog - 1)) < td.nrs,
-                  "stripe lanes more than needed for %d stripes", td.nrs);
-            std::vector<int> seen(static_cast<size_t>(td.nrs) * static_cast<size_t>(W), 0);
-            for (int t = 0; t < (1 << pl.fin_log2); ++t) {
-                const int c = t & (W - 1), lane = t >> (pl.fin_log2 - slog);
-                if (c >= it.count) continue;
-                for (int s0 = lane; s0 < td.nrs; s0 += S * kColLoads)
-                    for (int u = 0; u < kColLoads; ++u) {
-                        const int st = s0 + u * S;
-                        if (st >= td.nrs) continue;
-                        CHECK(int64_t(st) * td.n + it.start + c < int64_t(td.nrs) * td.n,
-                              "colpart read");
-                        seen[static_cast<size_t>(st) * W + c] += 1;
+            CHECK(it.count >= 1 && it.count <= 4 * T, "row item count");
+            CHECK(it.start % (4 * T) == 0 && it.chunk == td.chunk + it.start / kChunkRows,
+                  "row item alignment");
+            CHECK(it.f == td.r && it.len == td.m && it.part == td.rowpart && it.nparts == td.ncb,
+                  "row item descriptor");
+            const int64_t mp = pad4(td.m);
+            for (int t = 0; t < T; ++t) {
+                const int t0 = 4 * t;
+                if (t0 >= it.count) continue;
+                const int nv = it.count - t0 < 4 ? it.count - t0 : 4;
+                const int64_t i0 = int64_t(it.start) + t0;
+                for (int cb0 = 0; cb0 < td.ncb; cb0 += kFinRowLoads)
+                    for (int u = 0; u < kFinRowLoads; ++u) {
+                        const int cb = cb0 + u < td.ncb ? cb0 + u : td.ncb - 1;
+                        const int64_t off = int64_t(cb) * mp + i0;
+                        CHECK(off % 4 == 0 && off + 4 <= int64_t(td.ncb) * mp, "rowpart read");
+                        if (cb0 + u < td.ncb)
+                            for (int j = 0; j < nv; ++j)
+                                CHECK(rowp[static_cast<size_t>(it.tensor)]
+                                          .v[static_cast<size_t>(off + j)] == 1,
+                                      "rowpart read before written");
                     }
-                if (lane == 0) cols[static_cast<size_t>(it.tensor)].hit(int64_t(it.start) + c,
-                                                                      "column item column");
+                for (int j = 0; j < nv; ++j)
+                    rows[static_cast<size_t>(it.tensor)].hit(i0 + j, "row item row");
+            }
+            for (int w = 0; w < T / kWave; ++w)
+                if (w * kChunkRows < it.count)
+                    chunks[static_cast<size_t>(it.tensor)].hit(it.chunk - td.chunk + w, "chunk");
+        } else {
+            // thread t: columns 4(t mod 4) .. + 3 of group t / 4S, stripe
+            // lane (t / 4) mod S; every stripe of every column read once,
+            // each column updated once (by lane 0), and stripe lanes enough
+            // for at most kFinLoads stripes per thread unless that would
+            // leave less than one group per item.
+            CHECK(it.kind == FIN_COLS && q >= pl.row_items, "column item placement");
+            CHECK(it.f == td.c && it.len == td.n && it.part == td.colpart && it.nparts == td.nrs,
+                  "column item descriptor");
+            const int slog = it.lanes_log2, max_slog = pl.fin_log2 - 2;
+            CHECK(slog >= 0 && slog <= max_slog, "stripe lanes log2 %d", slog);
+            const int S = 1 << slog, ncol = 4 * (T >> slog);
+            CHECK(it.count >= 1 && it.count <= ncol && it.start % kColGroup == 0,
+                  "column item count %d cols %d start %d", it.count, ncol, it.start);
+            CHECK((int64_t(kFinLoads) << slog) >= td.nrs || slog == max_slog,
+                  "stripe lanes too few for %d stripes", td.nrs);
+            CHECK(slog == 0 || (int64_t(kFinLoads) << (slog - 1)) < td.nrs,
+                  "stripe lanes more than needed for %d stripes", td.nrs);
+            // the LDS fold past 16 stripe lanes: slots wave * 4 + c4 of the
+            // group's S / 16 waves, all inside the workgroup
+            if (S > kWave / 4) CHECK(T % (4 * S) == 0, "a group spans whole waves");
+            const int64_t csize = colpart_floats(td.n, td.nrs);
+            std::vector<int> seen(static_cast<size_t>(td.nrs) * static_cast<size_t>(ncol), 0);
+            for (int t = 0; t < T; ++t) {
+                const int c4 = t & 3, lane = (t >> 2) & (S - 1), g = t >> (2 + slog);
+                const int c0 = 16 * g + 4 * c4;
+                if (c0 >= it.count) continue;
+                const int64_t j0 = int64_t(it.start) + c0;
+                const int64_t base = colpart_index(j0, 0, td.nrs);
+                for (int s0 = lane; s0 < td.nrs; s0 += S * kFinLoads)
+                    for (int u = 0; u < kFinLoads; ++u) {
+                        const int st = s0 + u * S;
+                        const int stc = st < td.nrs ? st : td.nrs - 1;
+                        const int64_t off = base + int64_t(stc) * kColGroup;
+                        CHECK(off % 4 == 0 && off + 4 <= csize, "colpart read");
+                        if (st >= td.nrs) continue;
+                        for (int j = 0; j < 4 && c0 + j < it.count; ++j) {
+                            CHECK(off + j == colpart_index(j0 + j, st, td.nrs), "colpart layout");
+                            CHECK(colp[static_cast<size_t>(it.tensor)]
+                                      .v[static_cast<size_t>(off + j)] == 1,
+                                  "colpart read before written");
+                            seen[static_cast<size_t>(st) * ncol + c0 + j] += 1;
+                        }
+                    }
+                if (lane == 0)
+                    for (int j = 0; j < 4 && c0 + j < it.count; ++j)
+                        cols[static_cast<size_t>(it.tensor)].hit(j0 + j, "column item column");
             }
             for (int st = 0; st < td.nrs; ++st)
                 for (int c = 0; c < it.count; ++c)
-                    CHECK(seen[static_cast<size_t>(st) * W + c] == 1, "stripe %d column %d read %d times",
-                          st, c, seen[static_cast<size_t>(st) * W + c]);
+                    CHECK(seen[static_cast<size_t>(st) * ncol + c] == 1,
+                          "stripe %d column %d read %d times", st, c,
+                          seen[static_cast<size_t>(st) * ncol + c]);
         }
     }
     for (int64_t i = 0; i < count; ++i) {
@@ -241,8 +289,13 @@ static void check_plan(const Plan &pl, int64_t count)
         CHECK(elems[static_cast<size_t>(i)].all(), "tensor %lld (%lldx%lld) not fully covered",
               (long long)i, (long long)td.m, (long long)td.n);
         if (td.kind == KIND_MATRIX) {
-            CHECK(rowp[static_cast<size_t>(i)].all(), "row partials incomplete");
-            CHECK(colp[static_cast<size_t>(i)].all(), "column partials incomplete");
+            CHECK(rowp[static_cast<size_t>(i)].all_rows(pad4(td.m), td.m), "row partials incomplete");
+            bool cols_done = true;
+            for (int64_t st = 0; st < td.nrs; ++st)
+                for (int64_t j = 0; j < td.n; ++j)
+                    cols_done = cols_done && colp[static_cast<size_t>(i)]
+                                                 .v[static_cast<size_t>(colpart_index(j, st, td.nrs))];
+            CHECK(cols_done, "column partials incomplete");
             CHECK(chunks[static_cast<size_t>(i)].all(), "chunks incomplete");
             CHECK(rows[static_cast<size_t>(i)].all(), "row items incomplete");
             CHECK(cols[static_cast<size_t>(i)].all(), "column items incomplete");
