@@ -181,7 +181,7 @@ def time_adafm(specs, dtype, steps, warmup, seed=0, **hp):
     R.adafm_timing_enable(opt.ctx, True)
     for _ in range(steps):
         opt.step()
-    (stats, fin, rms, upd), n = R.adafm_timing_read(opt.ctx)
+    (stats, fin, rms, scale, upd), n = R.adafm_timing_read(opt.ctx)
     opt.close()
     del xs, gs
     torch.cuda.empty_cache()
@@ -189,10 +189,10 @@ def time_adafm(specs, dtype, steps, warmup, seed=0, **hp):
     return {"ms_per_step": ms, "params_per_s": sum(s.numel for s in specs) / (ms * 1e-3),
             "hbm_gbps_step": total / (ms * 1e-3) / 1e9, "min_bytes_per_step": total,
             "state_bytes": state,
-            "pass_ms": {"stats": stats / n, "finalize": fin / n, "rms_scale": rms / n,
-                        "update": upd / n},
+            "pass_ms": {"stats": stats / n, "finalize": fin / n, "rms": rms / n,
+                        "scale": scale / n, "update": upd / n},
             "stats_gbps": stats_b / (stats / n * 1e-3) / 1e9,
-            "rms_scale_gbps": rms_b / (rms / n * 1e-3) / 1e9,
+            "rms_gbps": rms_b / (rms / n * 1e-3) / 1e9,
             "update_gbps": upd_bytes / (upd / n * 1e-3) / 1e9}
 
 
@@ -533,7 +533,7 @@ def main():
         for nm in ("adafm_fp32", "adafm_bf16"):
             var[nm]["read_passes_vs_read_probe"] = {
                 "stats": var[nm]["stats_gbps"] / probes["read_only"],
-                "rms_scale": var[nm]["rms_scale_gbps"] / probes["read_only"]}
+                "rms": var[nm]["rms_gbps"] / probes["read_only"]}
         var["friction_report_wte"] = time_friction_report(50257, 768)
         var["launch_bound_sets"] = {
             "single_256x512_fp32": time_small(synth.single_matrix(), hp, 200, 5),

@@ -368,11 +368,12 @@ rikfad_status adafm_min_bytes(const adafm_ctx *ctx, int64_t *min_bytes_per_step,
                               int64_t *update_min_bytes, int64_t *state_bytes);
 /* 1 if a non-finite R or C value was produced since create (blocks). */
 rikfad_status adafm_nonfinite(adafm_ctx *ctx, void *stream, int32_t *out);
-/* Kernel timing as for rikfad_timing_*: ms4 = statistics pass, factor
- * finalisation, RMS pass + scale, update pass, summed over the timed
- * steps since the last read. */
+/* Kernel timing as for rikfad_timing_*: ms5[5] = statistics pass, factor
+ * finalisation, RMS pass (0 when clipping is off or there are no
+ * matrices), scale kernel, update pass, summed over the timed steps since
+ * the last read. */
 rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable);
-rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms4, int64_t *steps);
+rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms5, int64_t *steps);
 void adafm_destroy(adafm_ctx *ctx);
 
 /* ------------------------------------------------------------------------

@@ -350,13 +350,8 @@ struct StatsVec {
     }
 };
 
-// At least 6 waves per SIMD (three workgroups per CU): the 8-wide bf16
-// instantiation would otherwise take 83 registers and run two workgroups
-// per CU (statistics pass 5.4 against 5.7 TB/s on GPT2-S shapes); the
-// others fit anyway.  The RMS pass runs best as compiled (7 waves).
 template <typename XT, int V, bool X2>
-__global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(6)))
-void adafm_stats_kernel(
+__global__ __launch_bounds__(kStreamThreads) void adafm_stats_kernel(
     const TensorDesc *__restrict__ tensors, const void *const *__restrict__ grads,
     const Tile *__restrict__ tiles, int64_t tile0, float *__restrict__ ws,
     float *__restrict__ tilepart, AdaCoeffs k)
@@ -584,16 +579,13 @@ __global__ __launch_bounds__(kStreamThreads) void adafm_update_kernel(
 }
 
 // Kernel instantiation for a tile group's (storage type, width); a wide
-// one also serves the group's one-column tiles.  Only the read passes
-// (Wide8) have 8-wide bf16 groups.  nullptr for a combination the planner
-// does not produce.
-template <typename F, bool Wide8 = false, typename Pick>
+// one also serves the group's one-column tiles.  nullptr for a combination
+// the planner does not produce.
+template <typename F, typename Pick>
 F pick(const TileGroup &gr, Pick p)
 {
     if (gr.dtype == DT_F32) return gr.vec == 4 ? p.template get<float, 4>()
                                 : gr.vec == 1 ? p.template get<float, 1>() : nullptr;
-    if constexpr (Wide8)
-        if (gr.vec == 8) return p.template get<uint16_t, 8>();
     return gr.vec == 4 ? p.template get<uint16_t, 4>()
          : gr.vec == 1 ? p.template get<uint16_t, 1>() : nullptr;
 }
@@ -626,8 +618,8 @@ hipError_t launch_adafm_stats(const TensorDesc *tensors, const void *const *grad
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
-        const StatsFn fn = x2 ? pick<StatsFn, true>(gr, PickStats<true>())
-                              : pick<StatsFn, true>(gr, PickStats<false>());
+        const StatsFn fn = x2 ? pick<StatsFn>(gr, PickStats<true>())
+                              : pick<StatsFn>(gr, PickStats<false>());
         if (!fn) return hipErrorInvalidValue;
         hipEvent_t a = start, b = q == last ? stop : nullptr;
         start = nullptr;
@@ -648,7 +640,7 @@ hipError_t launch_adafm_rms(const TensorDesc *tensors, const void *const *grads,
     for (int q = 0; q < ngroups; ++q) {
         const TileGroup &gr = groups[q];
         if (gr.count <= 0) continue;
-        const RmsFn fn = pick<RmsFn, true>(gr, PickRms());
+        const RmsFn fn = pick<RmsFn>(gr, PickRms());
         if (!fn) return hipErrorInvalidValue;
         hipEvent_t a = start, b = q == last ? stop : nullptr;
         start = nullptr;

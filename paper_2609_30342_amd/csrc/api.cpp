@@ -203,18 +203,12 @@ constexpr int kUpdateRowsPerWave = 3;   // Adafactor-m update pass (see adafm_ct
 // the chip.
 constexpr int kReadRowsPerWave = RK_ADA_READ_ROWS;
 constexpr int64_t kReadMinTiles = 512;
-#ifndef RK_ADA_BF16_READ_VEC
-#define RK_ADA_BF16_READ_VEC 8
-#endif
-// bf16 elements per lane in the read passes: 8 (16-byte loads of g, 1 KB
-// per wave and row) where the rows allow it.
-constexpr int kReadBf16Vec = RK_ADA_BF16_READ_VEC;
 
 struct adafm_ctx {
     rk::Plan plan;
     DeviceTables dev;
     GradRing ring;
-    Timing timing{4};          // statistics, finalisation, RMS + scale, update
+    Timing timing{5};          // statistics, finalisation, RMS pass, scale, update
     adafm_hparams hp{};
     int64_t steps = 0;                      // steps taken
     std::vector<rk::TensorRange> ranges;    // tiles of each tensor
@@ -689,13 +683,12 @@ rikfad_status adafm_create(const rikfad_tensor *tensors, int64_t count, const ad
     adafm_ctx *ctx = new (std::nothrow) adafm_ctx();
     if (!ctx) return fail(RIKFAD_ENOMEM, "host allocation failed");
     std::string err;
-    if ((s = rk::plan_rikfad(tensors, count, ctx->plan, err, kReadRowsPerWave, kReadBf16Vec)) !=
-        RIKFAD_OK) {
+    if ((s = rk::plan_rikfad(tensors, count, ctx->plan, err, kReadRowsPerWave)) != RIKFAD_OK) {
         delete ctx;
         return fail(s, err);
     }
     if (ctx->plan.matrix_tiles < kReadMinTiles &&
-        (s = rk::plan_rikfad(tensors, count, ctx->plan, err, 0, kReadBf16Vec)) != RIKFAD_OK) {
+        (s = rk::plan_rikfad(tensors, count, ctx->plan, err, 0)) != RIKFAD_OK) {
         delete ctx;
         return fail(s, err);
     }
@@ -762,20 +755,19 @@ rikfad_status adafm_step(adafm_ctx *ctx, void *stream_)
                                 fk, ctx->dev.flag, 0, stream, t0, t1);
         if (e != hipSuccess) return hip_fail(e, "launch finalize kernel");
     }
-    // RMS pass (when clipping and there are matrices) and the scale kernel:
-    // one timed phase from the first of them to the scale kernel.
-    if ((s = tm.phase(2, &t0, &t1)) != RIKFAD_OK) return s;
+    // RMS pass (when clipping and there are matrices), then the scale kernel.
     if (ctx->hp.clip_threshold > 0 && pl.matrix_tiles > 0) {
+        if ((s = tm.phase(2, &t0, &t1)) != RIKFAD_OK) return s;
         e = rk::launch_adafm_rms(ctx->dev.tensors, ctx->dev.grads, ctx->dev.tiles,
                                  pl.groups.data(), ng, ctx->dev.ws, ctx->tilepart, stream, t0,
-                                 nullptr);
+                                 t1);
         if (e != hipSuccess) return hip_fail(e, "launch adafm rms kernel");
-        t0 = nullptr;
     }
+    if ((s = tm.phase(3, &t0, &t1)) != RIKFAD_OK) return s;
     e = rk::launch_adafm_scale(ctx->ranges_dev, static_cast<int64_t>(pl.tensors.size()),
                                ctx->tilepart, ctx->scales, k, stream, t0, t1);
     if (e != hipSuccess) return hip_fail(e, "launch adafm scale kernel");
-    if ((s = tm.phase(3, &t0, &t1)) != RIKFAD_OK) return s;
+    if ((s = tm.phase(4, &t0, &t1)) != RIKFAD_OK) return s;
     e = rk::launch_adafm_update(ctx->dev.tensors, ctx->dev.grads, ctx->upd_tiles,
                                 ctx->upd_groups.data(), static_cast<int>(ctx->upd_groups.size()),
                                 ctx->dev.ws, ctx->scales, k, stream, t0, t1);
@@ -859,10 +851,10 @@ rikfad_status adafm_timing_enable(adafm_ctx *ctx, int32_t enable)
     return RIKFAD_OK;
 }
 
-rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms4, int64_t *steps)
+rikfad_status adafm_timing_read(adafm_ctx *ctx, double *ms5, int64_t *steps)
 {
-    if (!ctx || !ms4 || !steps) return fail(RIKFAD_EINVAL, "NULL argument");
-    return read_timing(ctx->timing, ms4, steps);
+    if (!ctx || !ms5 || !steps) return fail(RIKFAD_EINVAL, "NULL argument");
+    return read_timing(ctx->timing, ms5, steps);
 }
 
 void adafm_destroy(adafm_ctx *ctx)

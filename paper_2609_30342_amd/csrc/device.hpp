@@ -179,23 +179,6 @@ template <> struct Raw<uint16_t, 4> {
     }
 };
 
-template <> struct Raw<uint16_t, 8> {
-    typedef u32x4 type;
-    static __device__ __forceinline__ type load(const uint16_t *q)
-    {
-        return ldg(reinterpret_cast<const u32x4 *>(q));
-    }
-    static __device__ __forceinline__ void unpack(const type &v, float (&o)[8])
-    {
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            o[2 * i] = __uint_as_float(w[i] << 16);
-            o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-        }
-    }
-};
-
 template <> struct Raw<uint16_t, 1> {
     typedef uint16_t type;
     static __device__ __forceinline__ type load(const uint16_t *q) { return ldg(q); }

@@ -119,9 +119,7 @@ struct Tile {
 // streaming kernel: the matrix tiles of one storage type (4-wide ones
 // first, then one-column ones, which the 4-wide instantiation also serves),
 // then that type's vector tiles.  vec (4, or 1 when the type has no 4-wide
-// matrix tile) selects the kernel instantiation.  A plan with 8-wide bf16
-// tiles (Adafactor-m read passes) has a bf16 group of width 8 (8-wide and
-// one-column tiles, vectors) and one of width 4 (4-wide tiles only).
+// matrix tile) selects the kernel instantiation.
 struct TileGroup {
     int32_t dtype;
     int32_t vec;

@@ -20,14 +20,11 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 // 128-bit path when rows stay 16-byte aligned, else narrower accesses.
-// bf16 matrices take 4 elements per lane (64-bit x and g accesses), or 8
-// (128-bit) when bf16_vec is 8 and the rows allow it.
-int32_t matrix_vec(const rikfad_tensor &t, int bf16_vec)
+// bf16 matrices take 4 elements per lane (64-bit x and g accesses).
+int32_t matrix_vec(const rikfad_tensor &t)
 {
     if (t.dtype == RIKFAD_FP32)
         return (t.n % 4 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16)) ? 4 : 1;
-    if (bf16_vec == 8 && t.n % 8 == 0 && aligned(t.x, 16) && aligned(t.g, 16) && aligned(t.p, 16))
-        return 8;
     if (t.n % 4 == 0 && aligned(t.x, 8) && aligned(t.g, 8) && aligned(t.p, 16)) return 4;
     return 1;
 }
@@ -159,12 +156,8 @@ int matrix_blocks(int64_t n, int32_t vec, int base, std::vector<Block> &blocks)
 }  // namespace
 
 rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::string &err,
-                          int rows_per_wave, int bf16_vec)
+                          int rows_per_wave)
 {
-    if (bf16_vec != 4 && bf16_vec != 8) {
-        err = "bf16 access width must be 4 or 8";
-        return RIKFAD_EINVAL;
-    }
     if (count < 0 || (count > 0 && !t)) {
         err = "tensor list is NULL or count < 0";
         return RIKFAD_EINVAL;
@@ -200,7 +193,7 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         for (int64_t i = 0; i < count; ++i) {
             const rikfad_tensor &T = t[i];
             if (T.m == 1 || T.n == 1) continue;
-            const int rpw = matrix_blocks(T.n, matrix_vec(T, bf16_vec), kRowsPerWave, blocks);
+            const int rpw = matrix_blocks(T.n, matrix_vec(T), kRowsPerWave, blocks);
             ntiles += static_cast<int64_t>(blocks.size()) *
                       ceil_div(T.m, int64_t(kStreamWaves) * rpw);
         }
@@ -215,11 +208,11 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
     int64_t ws = 0;
     pl.tensors.resize(static_cast<size_t>(count));
     pl.grads.resize(static_cast<size_t>(count));
-    // Matrix tiles by class (fp32 v4, fp32 v1, bf16 v8, bf16 v4, bf16 v1);
-    // vector tiles by dtype.
-    constexpr int kClasses = 5;
-    const int32_t class_dtype[kClasses] = {DT_F32, DT_F32, DT_BF16, DT_BF16, DT_BF16};
-    const int32_t class_vec[kClasses] = {4, 1, 8, 4, 1};
+    // Matrix tiles by class (fp32 v4, fp32 v1, bf16 v4, bf16 v1); vector
+    // tiles by dtype.
+    constexpr int kClasses = 4;
+    const int32_t class_dtype[kClasses] = {DT_F32, DT_F32, DT_BF16, DT_BF16};
+    const int32_t class_vec[kClasses] = {4, 1, 4, 1};
     std::vector<Tile> mat_tiles[kClasses];
     std::vector<Tile> vec_tiles[2];
     std::vector<FinItem> col_items;
@@ -254,7 +247,7 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
             continue;
         }
         d.kind = KIND_MATRIX;
-        d.vec = matrix_vec(T, bf16_vec);
+        d.vec = matrix_vec(T);
         pl.matrices += 1;
         pl.state_bytes += 4 * mn + 4 * (T.m + T.n);
         pl.min_bytes += mn * (3 * eb + 8) + 8 * (T.m + T.n);   // x g p in, x p out; R C
@@ -339,11 +332,9 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
                                  static_cast<int32_t>(d.n - j0 < cols ? d.n - j0 : cols), d.nrs,
                                  slog});
     }
-    // One launch per storage type: its widest matrix tiles, then its
+    // One launch per storage type: its 4-wide matrix tiles, then its
     // one-column matrix tiles (served by the same launch), then its vector
-    // tiles; the group's width selects the kernel instantiation.  With
-    // 8-wide bf16 tiles, bf16 matrices whose rows only allow 4 elements per
-    // lane get a second bf16 launch of their own.
+    // tiles; the group's width selects the kernel instantiation.
     auto add_group = [&](int32_t dtype, int32_t vec, std::initializer_list<int> classes,
                          bool vectors) {
         TileGroup gr{dtype, vec, static_cast<int64_t>(pl.tiles.size()), 0};
@@ -359,12 +350,7 @@ rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &pl, std::
         if (gr.count > 0) pl.groups.push_back(gr);
     };
     add_group(DT_F32, mat_tiles[0].empty() ? 1 : 4, {0, 1}, true);
-    if (!mat_tiles[2].empty()) {
-        add_group(DT_BF16, 8, {2, 4}, true);
-        add_group(DT_BF16, 4, {3}, false);
-    } else {
-        add_group(DT_BF16, mat_tiles[3].empty() ? 1 : 4, {3, 4}, true);
-    }
+    add_group(DT_BF16, mat_tiles[2].empty() ? 1 : 4, {2, 3}, true);
     pl.row_items = static_cast<int64_t>(pl.fin.size());
     pl.fin.insert(pl.fin.end(), col_items.begin(), col_items.end());
     pl.ws_floats = ws;

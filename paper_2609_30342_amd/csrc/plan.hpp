@@ -29,12 +29,9 @@ struct Plan {
 // code with a message in `err`.
 // rows_per_wave > 0 fixes the rows per wave of every matrix tile (narrow
 // blocks still scale it up); 0 takes kRowsPerWave, halved for sets with
-// fewer matrix tiles than the chip has compute units.  bf16_vec (4 or 8):
-// elements per lane of bf16 matrix tiles whose rows allow 16-byte accesses;
-// only the Adafactor-m read passes, which load g (and x) and store neither,
-// use 8.
+// fewer matrix tiles than the chip has compute units.
 rikfad_status plan_rikfad(const rikfad_tensor *t, int64_t count, Plan &out, std::string &err,
-                          int rows_per_wave = 0, int bf16_vec = 4);
+                          int rows_per_wave = 0);
 
 // Validates and plans a full-tensor iKFAD context (every tensor element-wise).
 rikfad_status plan_ikfad(const ikfad_tensor *t, int64_t count, Plan &out, std::string &err);

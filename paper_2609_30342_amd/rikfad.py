@@ -356,9 +356,9 @@ def adafm_timing_enable(ctx, enable=True):
 
 
 def adafm_timing_read(ctx):
-    """(ms of the statistics pass, finalisation, RMS pass + scale, update
-    pass) summed over the timed steps, and the step count."""
-    ms = (ctypes.c_double * 4)()
+    """(ms of the statistics pass, finalisation, RMS pass, scale kernel,
+    update pass) summed over the timed steps, and the step count."""
+    ms = (ctypes.c_double * 5)()
     steps = ctypes.c_int64()
     _check(lib().adafm_timing_read(ctx, ms, ctypes.byref(steps)), "adafm_timing_read")
     return tuple(ms), steps.value

@@ -162,28 +162,20 @@ static void check_plan(const Plan &pl, int64_t count)
     // groups partition the tile table, one group per storage type; a
     // group's matrix tiles are its own width or one-column (served by the
     // same instantiation), and a one-column group holds no wider tile.
-    // Exception: a plan with 8-wide bf16 tiles has a bf16 group of width 8
-    // followed by one of width 4 that holds only 4-wide matrix tiles.
     int64_t covered = 0;
     int ngroups[2] = {0, 0};
-    int first_vec[2] = {0, 0};
     for (const TileGroup &g : pl.groups) {
         CHECK(g.begin == covered, "groups not contiguous");
         CHECK(g.count > 0, "empty group");
         const int dt = g.dtype == DT_F32 ? 0 : 1;
-        CHECK(g.vec == 4 || g.vec == 1 || (g.vec == 8 && dt == 1), "group width %d", g.vec);
-        const bool second = ngroups[dt] == 1;
-        CHECK(ngroups[dt] == 0 || (second && dt == 1 && first_vec[dt] == 8 && g.vec == 4),
-              "two groups of one storage type");
-        if (ngroups[dt] == 0) first_vec[dt] = g.vec;
+        CHECK(g.vec == 4 || g.vec == 1, "group width %d", g.vec);
+        CHECK(ngroups[dt] == 0, "two groups of one storage type");
         ++ngroups[dt];
         covered += g.count;
         for (int64_t t = g.begin; t < g.begin + g.count; ++t) {
             const Tile &tl = pl.tiles[static_cast<size_t>(t)];
             CHECK(tl.dtype == g.dtype, "tile dtype vs group");
-            if (second) CHECK(tl.kind == KIND_MATRIX && tl.vec == 4, "second bf16 group");
-            else if (tl.kind == KIND_MATRIX)
-                CHECK(tl.vec == g.vec || tl.vec == 1, "tile vec vs group");
+            if (tl.kind == KIND_MATRIX) CHECK(tl.vec == g.vec || tl.vec == 1, "tile vec vs group");
         }
     }
     CHECK(covered == static_cast<int64_t>(pl.tiles.size()), "groups do not cover tiles");
@@ -430,23 +422,13 @@ int main(int argc, char **argv)
         for (const Tile &tl : pu.tiles)
             if (tl.kind == KIND_MATRIX && tl.lanes_log2 == 6)
                 CHECK(tl.rpw == 3, "full-width tile with %d rows per wave, not 3", tl.rpw);
-        // its read passes plan it with 16 rows per wave and 8-wide bf16
-        // tiles where the rows allow them (also with the default rows)
+        // its read passes plan it with 16 rows per wave (and with the
+        // default rows, for sets too small for that)
         for (int rows : {16, 0}) {
             Plan pr;
-            CHECK(plan_rikfad(ts.data(), count, pr, err, rows, 8) == RIKFAD_OK,
+            CHECK(plan_rikfad(ts.data(), count, pr, err, rows) == RIKFAD_OK,
                   "plan (read passes, %d rows): %s", rows, err.c_str());
             check_plan(pr, count);
-            for (const Tile &tl : pr.tiles) {
-                if (tl.kind != KIND_MATRIX || tl.dtype != DT_BF16) continue;
-                const TensorDesc &td = pr.tensors[static_cast<size_t>(tl.tensor)];
-                const rikfad_tensor &T = ts[static_cast<size_t>(tl.tensor)];
-                const bool a16 = (reinterpret_cast<uintptr_t>(T.x) % 16 == 0) &&
-                                 (reinterpret_cast<uintptr_t>(T.g) % 16 == 0) &&
-                                 (reinterpret_cast<uintptr_t>(T.p) % 16 == 0);
-                CHECK((tl.vec == 8) == (td.n % 8 == 0 && a16), "bf16 read width %d for n %lld",
-                      tl.vec, (long long)td.n);
-            }
         }
     }
     std::printf("plan_check: %d plans checked, %d rejected as expected, %d failures\n", planned,

@@ -87,6 +87,9 @@ def test_ikfad_and_adafm_timing():
         R.adafm_timing_enable(opt.ctx, True)
         for _ in range(3):
             opt.step()
-        ms4, n = R.adafm_timing_read(opt.ctx)
-        assert n == 3 and all(t > 0.0 for t in ms4), ms4    # RMS phase: scale kernel at least
+        ms5, n = R.adafm_timing_read(opt.ctx)
+        assert n == 3, n
+        stats, fin, rms, scale, upd = ms5
+        assert stats > 0.0 and fin > 0.0 and scale > 0.0 and upd > 0.0, ms5
+        assert (rms > 0.0) == (clip > 0.0), ms5       # no RMS pass without clipping
         opt.close()
