@@ -103,7 +103,7 @@ EDGE = [
     ("narrow_L1", [S("a", 3, 4)]),
     ("tiny", [S("a", 5, 6), S("b", 2, 2), S("c", 2, 3)]),
     ("vectors", [S("v", 1, 1000), S("w", 1000, 1), S("s", 1, 1), S("u", 1, 7)]),
-    ("bf16_v8", [S("a", 200, 776, "bf16")]),                 # 97 lanes: 64 + 33 (L = 64)
+    ("bf16_776", [S("a", 200, 776, "bf16")]),                # 194 lanes: 3 blocks + 2 (L = 2)
     ("bf16_v4", [S("a", 64, 36, "bf16")]),
     ("bf16_v1", [S("a", 65, 27, "bf16"), S("b", 1, 33, "bf16")]),
     ("tall", [S("a", 3000, 12)]),                            # many stripes, 3 lanes per row
@@ -155,19 +155,25 @@ def test_random_sets(seed):
 
 
 # Column items split their T threads (256, or 1024 when a matrix has more
-# than 512 row stripes) into S stripe lanes x T / S columns, S the smallest
-# power of two leaving each thread at most 32 row stripes (at least 16
-# columns per item): S = 1 at 32 stripes (1024 rows), S = 2 at 33 (1056
-# rows), S = 4 at 66-71 stripes, S = 64 with two batches of loads per
-# thread at 2188 stripes (70000 rows).
+# than 512 row stripes) into S stripe lanes of T / S threads with 4 columns
+# each, S the smallest power of two leaving each thread at most 8 row
+# stripes (at least one 16-column group per item); up to 16 stripe lanes
+# fold inside a wave, more through LDS.  These sets are small (fewer tiles
+# than compute units: 16-row stripes) except "mixed" and the last two:
+# S = 8 at 64 stripes (1024 rows), S = 16 at 66 (1056 rows, and "mixed"),
+# S = 32 at 132-141, S = 64 at 300 (the cap of 256-thread items: one
+# 16-column group each), S = 128 at 625 (20000 rows), and S = 256 with two
+# batches of loads per thread at 2188 stripes (70000 rows).  The edge
+# shapes above cover S = 1, 2 and 4.
 COLUMN_CASES = [
-    ("s1_32_stripes", [S("a", 1024, 300)], 12),
-    ("s2_33_stripes", [S("a", 1056, 300)], 12),
-    ("tall_s4", [S("a", 9000, 64), S("b", 4200, 96, "bf16")], 12),
+    ("s8_64_stripes", [S("a", 1024, 300)], 12),
+    ("s16_66_stripes", [S("a", 1056, 300)], 12),
+    ("tall_s32", [S("a", 9000, 64), S("b", 4200, 96, "bf16")], 12),
     ("mixed", [S("a", 96, 200), S("b", 1, 200), S("c", 40, 640, "bf16"), S("d", 640, 1, "bf16"),
                S("e", 2100, 1000)], 12),
-    ("s64_two_batches", [S("a", 70000, 256), S("b", 1, 256)], 5),
-    # 625 stripes: 1024-thread items of 32 stripe lanes x 32 columns, the
+    ("s64_cap_256_threads", [S("a", 9600, 256)], 6),
+    ("s256_two_batches", [S("a", 70000, 256), S("b", 1, 256)], 5),
+    # 625 stripes: 1024-thread items of 128 stripe lanes x 32 columns, the
     # last of 8 columns; the one-column-path matrix shares the launch size
     ("ragged_1024_threads", [S("a", 20000, 1000), S("b", 300, 27)], 4),
 ]
