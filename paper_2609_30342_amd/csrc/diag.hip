@@ -107,8 +107,8 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
 }
 
 // One pass over xi for n <= 64 * NC, reading xi once: a workgroup takes
-// kPowRows rows, each wave a quarter of them in order.  Lane l holds
-// columns l, l + 64, ... of a row in registers; the wave forms the row's
+// kPowRows rows, each of its kPowWaves waves an equal share in order.  Lane
+// l holds columns l, l + 64, ... of a row in registers; the wave forms the row's
 // weighted sum s_i = sum_j xi[i, j] w_j (lanes in column order, then the
 // butterfly) and adds xi[i, j] times a row weight to its column
 // accumulators, rows in order.  The waves' column sums are added in wave
@@ -122,23 +122,32 @@ __global__ __launch_bounds__(kT) void row_reduce_kernel(const float *__restrict_
 //                  with xi~_ij = R_i C_j / (1^T R + eps) (0 if that is 0)
 //   kPassNorm      kPassPower, plus spart[0] = sum u_i^2
 // Shape of the one-pass kernels, measured on the 50257 x 768 report (30
-// iterations): 128 rows per workgroup (64: 1.57 ms, 256: 1.34 ms), and
-// the load of row i + 1 issued before row i is reduced (more rows ahead
+// iterations): 8 waves of 32 rows each (256 rows per workgroup), which
+// halves the column partial sums of 4 waves of 32 rows: 1.085-1.089
+// against 1.118-1.150 ms (8 waves of 24 rows: 1.52 ms).  With 4 waves,
+// 32 rows per wave beat 16 and 64 (1.19 against 1.57 and 1.34 ms).  The
+// load of row i + 1 is issued before row i is reduced (more rows ahead
 // measured slower: 2 rows 1.19-1.21 ms, 3 rows 1.25, 4 rows 1.30, against
-// 1.19 ms).
+// 1.19 ms, with 4 waves).
 #ifndef RK_DIAG_POW_ROWS
-#define RK_DIAG_POW_ROWS 128
+#define RK_DIAG_POW_ROWS 256
 #endif
 #ifndef RK_DIAG_POW_RING
 #define RK_DIAG_POW_RING 1
 #endif
+#ifndef RK_DIAG_POW_WAVES
+#define RK_DIAG_POW_WAVES 8
+#endif
 constexpr int kPowRows = RK_DIAG_POW_ROWS;   // rows per workgroup
 constexpr int kPowRing = RK_DIAG_POW_RING;   // rows loaded ahead per wave
+constexpr int kPowWaves = RK_DIAG_POW_WAVES; // waves per workgroup
+constexpr int kPowThreads = 64 * kPowWaves;
+static_assert(kPowRows % kPowWaves == 0, "whole rows per wave");
 static_assert(kErrRows <= kPowRows, "the error partials hold one pair per one-pass workgroup");
 enum : int { kPassSums = 0, kPassPower = 1, kPassPowerErr = 2, kPassNorm = 3 };
 
 template <int NC, int MODE>
-__global__ __launch_bounds__(kT) void onepass_kernel(
+__global__ __launch_bounds__(kPowThreads) void onepass_kernel(
     const float *__restrict__ xi, int64_t m, int64_t n, const double *__restrict__ v,
     const double *__restrict__ vparts, int64_t nvparts, const double *__restrict__ r,
     const double *__restrict__ c, const double *__restrict__ stats_r, double eps,
@@ -146,8 +155,8 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
 {
     constexpr bool kWeighted = MODE != kPassSums;
     constexpr bool kErr = MODE == kPassPowerErr;
-    __shared__ double l[kT / 64][64 * NC];
-    __shared__ double ls[kT / 64][2];
+    __shared__ double l[kPowWaves][64 * NC];
+    __shared__ double ls[kPowWaves][2];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const double scale = kWeighted ? inv_norm(vparts, nvparts) : 1.0;
     // Every load below is unconditional, its address clamped into the
@@ -169,8 +178,8 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
         const double denom = gp(stats_r)[1] + eps;
         inv = denom == 0.0 ? 0.0 : 1.0 / denom;
     }
-    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kPowRows + wave * (kPowRows / 4);
-    const int64_t r1 = r0 + kPowRows / 4 < m ? r0 + kPowRows / 4 : m;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kPowRows + wave * (kPowRows / kPowWaves);
+    const int64_t r1 = r0 + kPowRows / kPowWaves < m ? r0 + kPowRows / kPowWaves : m;
     const int64_t rlast = r1 - 1;       // a row of xi (m >= 1), the wave's last if it has rows
     auto load_row = [&](int64_t row, float (&dst)[NC], double &rr) {
         const int64_t rc = row < r1 ? row : rlast;
@@ -231,16 +240,16 @@ __global__ __launch_bounds__(kT) void onepass_kernel(
         }
     }
     __syncthreads();
-    for (int64_t j = threadIdx.x; j < n; j += kT) {
+    for (int64_t j = threadIdx.x; j < n; j += kPowThreads) {
         double s = l[0][j];
 #pragma unroll
-        for (int w = 1; w < kT / 64; ++w) s += l[w][j];
+        for (int w = 1; w < kPowWaves; ++w) s += l[w][j];
         gp(part)[static_cast<int64_t>(blockIdx.x) * n + j] = s;
     }
     if ((kErr || MODE == kPassNorm) && threadIdx.x == 0) {
         double a = ls[0][0], b = ls[0][1];
 #pragma unroll
-        for (int w = 1; w < kT / 64; ++w) {
+        for (int w = 1; w < kPowWaves; ++w) {
             a += ls[w][0];
             b += ls[w][1];
         }
@@ -520,13 +529,13 @@ template <int MODE, typename... Args>
 void launch_onepass(int nc, dim3 grid, hipStream_t st, Args... args)
 {
     if (nc == 4)
-        hipLaunchKernelGGL((onepass_kernel<4, MODE>), grid, dim3(kT), 0, st, args...);
+        hipLaunchKernelGGL((onepass_kernel<4, MODE>), grid, dim3(kPowThreads), 0, st, args...);
     else if (nc == 8)
-        hipLaunchKernelGGL((onepass_kernel<8, MODE>), grid, dim3(kT), 0, st, args...);
+        hipLaunchKernelGGL((onepass_kernel<8, MODE>), grid, dim3(kPowThreads), 0, st, args...);
     else if (nc == 12)
-        hipLaunchKernelGGL((onepass_kernel<12, MODE>), grid, dim3(kT), 0, st, args...);
+        hipLaunchKernelGGL((onepass_kernel<12, MODE>), grid, dim3(kPowThreads), 0, st, args...);
     else
-        hipLaunchKernelGGL((onepass_kernel<16, MODE>), grid, dim3(kT), 0, st, args...);
+        hipLaunchKernelGGL((onepass_kernel<16, MODE>), grid, dim3(kPowThreads), 0, st, args...);
 }
 
 // The report itself on a workspace of sh.words doubles at buf (device
