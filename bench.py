@@ -338,6 +338,18 @@ def time_probe_mix(nelem, dtype, shape, reps=50):
     return per * nelem / (ms * 1e-3) / 1e9
 
 
+def time_probe_write(nbytes, reps=50):
+    """Write-only stream of nbytes.  GB/s."""
+    import torch
+    from paper_2609_30342_amd import rikfad as R
+    a = torch.empty(nbytes // 4, device="cuda:0")
+    s = torch.cuda.current_stream().cuda_stream
+    ms = _time_calls(lambda: R.rikfad_probe_write(a.data_ptr(), nbytes, 0x3f800000, s), reps)
+    del a
+    torch.cuda.empty_cache()
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 def time_probe_read(nbytes, reps=50):
     """Read-only stream of nbytes.  GB/s."""
     import torch
@@ -514,6 +526,7 @@ def main():
         probes = {f"mix_{dt}_{nm}": time_probe_mix(N, dt, sh)
                   for dt in ("fp32", "bf16") for sh, nm in ((0, "contig"), (1, "tiles"))}
         probes["read_only"] = time_probe_read(4 * N)
+        probes["write_only"] = time_probe_write(4 * N)
         var["probes_gbps"] = probes
         ceil = {dt: max(probes[f"mix_{dt}_contig"], probes[f"mix_{dt}_tiles"],
                         *( [var["probe_3r2w_gbps"]] if dt == "fp32" else []))

@@ -397,6 +397,9 @@ void adafm_destroy(adafm_ctx *ctx);
  *     == 0) in four 16-byte loads per lane; writes *out (one float) only in
  *     the event that a workgroup's sum has one particular NaN bit pattern,
  *     which finite data never produces -- a read-only stream.
+ *   rikfad_probe_write: fills nbytes at dst (16-byte aligned, nbytes % 16
+ *     == 0) with the 32-bit pattern `value`, four 16-byte non-temporal
+ *     stores per lane -- a write-only stream.
  * ---------------------------------------------------------------------- */
 rikfad_status rikfad_probe_stream(const float *a, const float *b, const float *c,
                                   float *d, float *e, int64_t nfloat, void *stream);
@@ -406,6 +409,7 @@ rikfad_status rikfad_probe_mix(void *x, const void *g, float *p, int64_t nelem,
                                int32_t dtype, int32_t shape, void *stream);
 rikfad_status rikfad_probe_read(const void *src, int64_t nbytes, float *out,
                                 void *stream);
+rikfad_status rikfad_probe_write(void *dst, int64_t nbytes, uint32_t value, void *stream);
 
 #ifdef __cplusplus
 }

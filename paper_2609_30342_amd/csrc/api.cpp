@@ -906,6 +906,16 @@ rikfad_status rikfad_probe_read(const void *src, int64_t nbytes, float *out, voi
     return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_read");
 }
 
+rikfad_status rikfad_probe_write(void *dst, int64_t nbytes, uint32_t value, void *stream)
+{
+    if (!dst || nbytes < 0 || nbytes % 16 != 0)
+        return fail(RIKFAD_EINVAL, "probe_write: NULL pointer or nbytes not a multiple of 16");
+    if (reinterpret_cast<uintptr_t>(dst) % 16)
+        return fail(RIKFAD_EALIGN, "probe_write: dst must be 16-byte aligned");
+    hipError_t err = rk::launch_probe_write(dst, nbytes, value, static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? RIKFAD_OK : hip_fail(err, "launch probe_write");
+}
+
 rikfad_status rikfad_probe_copy(const void *src, void *dst, int64_t nbytes, void *stream)
 {
     auto al = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) % 16) == 0; };

@@ -669,6 +669,20 @@ __global__ __launch_bounds__(kThreads) void probe_read_kernel(const f32x4 *__res
     if (__float_as_uint(s) == kProbeSentinel) gmem(out)[0] = s;
 }
 
+// Write-only stream: four 16-byte non-temporal stores of one 32-bit
+// pattern per lane (the streams' store kind).
+__global__ __launch_bounds__(kThreads) void probe_write_kernel(u32x4 *__restrict__ a, int64_t n16,
+                                                               uint32_t value)
+{
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kThreads * kProbeUnroll + threadIdx.x;
+    const u32x4 v = {value, value, value, value};
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+        const int64_t i = base + static_cast<int64_t>(u) * kThreads;
+        if (i < n16) stg(a + i, v);
+    }
+}
+
 // ------------------------------------------------------------- launchers
 
 hipError_t launch_stream(const TensorDesc *tensors, const void *const *grads, const Tile *tiles,
@@ -796,6 +810,15 @@ hipError_t launch_probe_read(const void *a, int64_t nbytes, float *out, hipStrea
     if (n16 <= 0) return hipSuccess;
     hipLaunchKernelGGL(probe_read_kernel, dim3(probe_grid(n16)), dim3(kThreads), 0, stream,
                        static_cast<const f32x4 *>(a), n16, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_write(void *dst, int64_t nbytes, uint32_t value, hipStream_t stream)
+{
+    const int64_t n16 = nbytes / 16;
+    if (n16 <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_write_kernel, dim3(probe_grid(n16)), dim3(kThreads), 0, stream,
+                       static_cast<u32x4 *>(dst), n16, value);
     return hipGetLastError();
 }
 

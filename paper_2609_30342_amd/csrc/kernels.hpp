@@ -42,6 +42,7 @@ void set_last_error(const char *msg);
 hipError_t launch_probe_mix(void *x, const void *g, float *p, int64_t nelem, int dtype,
                             int shape, hipStream_t stream);
 hipError_t launch_probe_read(const void *a, int64_t nbytes, float *out, hipStream_t stream);
+hipError_t launch_probe_write(void *dst, int64_t nbytes, uint32_t value, hipStream_t stream);
 hipError_t launch_probe_copy(const void *s, void *d, int64_t nbytes, hipStream_t stream);
 
 }  // namespace rk

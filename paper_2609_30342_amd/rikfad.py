@@ -116,6 +116,7 @@ _SIGNATURES = {
     "rikfad_probe_copy": (_st, [_vp, _vp, _i64, _vp]),
     "rikfad_probe_mix": (_st, [_vp, _vp, _vp, _i64, _i32, _i32, _vp]),
     "rikfad_probe_read": (_st, [_vp, _i64, _vp, _vp]),
+    "rikfad_probe_write": (_st, [_vp, _i64, ctypes.c_uint32, _vp]),
 }
 
 
@@ -298,6 +299,11 @@ def rikfad_probe_mix(x, g, p, nelem, dtype, shape, stream=None):
 
 def rikfad_probe_read(src, nbytes, out, stream=None):
     _check(lib().rikfad_probe_read(src, int(nbytes), out, stream), "rikfad_probe_read")
+
+
+def rikfad_probe_write(dst, nbytes, value, stream=None):
+    _check(lib().rikfad_probe_write(dst, int(nbytes), int(value) & 0xffffffff, stream),
+           "rikfad_probe_write")
 
 
 def adafm_params(h, beta1=0.9, decay_rate=-0.8, eps1=1e-30, eps2=1e-3, clip_threshold=1.0,

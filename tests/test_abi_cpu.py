@@ -144,6 +144,9 @@ def test_probes_validate_arguments():
     assert L.rikfad_probe_mix(BASE + 8, BASE, BASE, 256, R.RIKFAD_FP32, 0, None) == R.RIKFAD_EALIGN
     assert L.rikfad_probe_read(BASE, 17, BASE, None) == R.RIKFAD_EINVAL
     assert L.rikfad_probe_read(BASE + 4, 32, BASE, None) == R.RIKFAD_EALIGN
+    assert L.rikfad_probe_write(BASE, 17, 0, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_write(None, 32, 0, None) == R.RIKFAD_EINVAL
+    assert L.rikfad_probe_write(BASE + 4, 32, 0, None) == R.RIKFAD_EALIGN
 
 
 def _specs_to_tensors(specs):

@@ -809,6 +809,16 @@ def test_mix_probe_computes_what_it_claims(dtype, shape):
     assert torch.equal(p, p0 * 0.5)
 
 
+def test_write_probe_fills_exactly_its_bytes():
+    n = (1 << 20) + 12                      # a ragged last workgroup
+    a = torch.zeros(n + 8, device="cuda")
+    R.rikfad_probe_write(a.data_ptr(), 4 * n, 0x3f800000,
+                         torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.all(a[:n] == 1.0)
+    assert torch.all(a[n:] == 0.0)
+
+
 def test_read_probe_reads_without_writing():
     n = (1 << 20) + 12
     a = torch.randn(n, device="cuda")
