@@ -278,3 +278,13 @@ def test_noalloc_friction_report_rejects_tensors_beyond_its_workspace():
                                             ctypes.byref(out)) == R.RIKFAD_EINVAL
     assert L.rikfad_friction_report_noalloc(BASE + 2, 8, 8, 0.0, 10, None,
                                             ctypes.byref(out)) == R.RIKFAD_EALIGN
+
+
+def test_c_program_builds_against_the_header():
+    """tests/c_abi_step.c compiles as C11 against include/rikfad.h and links
+    the library; without a GPU it stops before any library call (exit 77)."""
+    import subprocess
+    import cdriver
+    exe = cdriver.build()
+    r = subprocess.run([exe, "1", "1"], capture_output=True, text=True, timeout=60)
+    assert r.returncode in (0, 77), r.stdout + r.stderr
