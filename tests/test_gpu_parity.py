@@ -553,6 +553,46 @@ def test_deterministic_bitwise():
             assert torch.equal(u, v)
 
 
+def test_two_contexts_on_two_streams_bitwise():
+    """Two contexts stepped at the same time on two streams give, bit for
+    bit, what each gives when it runs alone: a context's tables, workspace,
+    flag and pending state are its own."""
+    specs_b = [S("f", 640, 768), S("g", 1, 768), S("h", 96, 2048, "bf16"), S("k", 33, 27)]
+    hp = synth.HP_FRICTION
+    log("[case] two contexts on two streams")
+
+    def run(concurrent):
+        a = make_pair(SPECS_MIX, hp, seed=5, checked=[])
+        b = make_pair(specs_b, hp, seed=7, checked=[])
+        load_grads(a, 0, 5)
+        load_grads(b, 0, 7)
+        torch.cuda.synchronize()
+        sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+        if concurrent:
+            for _ in range(8):
+                a.opt.step(stream=sa)
+                b.opt.step(stream=sb)
+        else:
+            for _ in range(8):
+                a.opt.step(stream=sa)
+            torch.cuda.synchronize()
+            for _ in range(8):
+                b.opt.step(stream=sb)
+        a.opt.sync_momentum(stream=sa)
+        b.opt.sync_momentum(stream=sb)
+        torch.cuda.synchronize()
+        assert not a.opt.nonfinite() and not b.opt.nonfinite()
+        return a, b
+
+    seq = run(False)
+    par = run(True)
+    for u, v in zip(seq, par):
+        for i in range(len(u.specs)):
+            assert torch.equal(u.xs[i], v.xs[i]), (u.specs[i].name, "x")
+            for k, (su, sv) in enumerate(zip(u.opt.state[i], v.opt.state[i])):
+                assert torch.equal(su, sv), (u.specs[i].name, "prc"[k])
+
+
 def test_deferred_equals_two_pass_bitwise():
     """The deferred half-kick performs the same operations as the two-pass
     schedule, so after syncing the results agree bit for bit."""
