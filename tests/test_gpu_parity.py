@@ -154,6 +154,18 @@ def test_random_sets(seed):
     assert_ok(errs, label=f"random {seed}")
 
 
+def test_many_tiny_tensors():
+    """3,000 tensors of 1 to 40 rows and columns (vectors, one-column and
+    4-wide matrices, fp32 and bf16) in one context: one launch per storage
+    type over thousands of small tiles, against the oracle."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([11, 0x7E1])))
+    specs = [S(f"t{i}", int(rng.integers(1, 41)), int(rng.integers(1, 41)),
+               "bf16" if rng.random() < 0.4 else "fp32") for i in range(3000)]
+    log(f"[case] many tiny tensors: {len(specs)}, {sum(sp.numel for sp in specs)} elements")
+    _, errs = run_parity(specs, synth.HP_FRICTION, 4, seed=11, label="many tiny")
+    assert_ok(errs, label="many tiny")
+
+
 # Column items split their T threads (256, or 1024 when a matrix has more
 # than 512 row stripes) into S stripe lanes of T / S threads with 4 columns
 # each, S the smallest power of two leaving each thread at most 8 row
