@@ -151,6 +151,19 @@ def test_tinyvit_bf16():
     assert_ok(errs, label="tinyvit")
 
 
+def test_many_tiny_tensors():
+    """2,000 tensors of 1 to 40 rows and columns, fp32 and bf16, with
+    clipping and parameter scaling on: per-tensor RMS and scale over
+    thousands of small tiles, against the oracle."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([13, 0xADA])))
+    specs = [S(f"t{i}", int(rng.integers(1, 41)), int(rng.integers(1, 41)),
+               "bf16" if rng.random() < 0.4 else "fp32") for i in range(2000)]
+    log(f"[case] adafm many tiny tensors: {len(specs)}")
+    hp = dict(HP, clip_threshold=0.5, scale_parameter=True)
+    _, errs = run_adafm_parity(specs, hp, 4, seed=13, label="many tiny")
+    assert_ok(errs, label="adafm many tiny")
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_gpt2_small_full_size(dtype):
     """GPT2-S-shaped set at full size in one context (the benchmark's
