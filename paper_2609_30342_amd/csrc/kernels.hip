@@ -38,8 +38,8 @@ __device__ __forceinline__ float row_rate(float kh, float r_i, float denom)
 
 // ------------------------------------------------ streaming pass (matrix)
 //
-// A tile is 4 x rpw rows x one column block.  Each wave walks rpw
-// consecutive rows; a row of the block is covered by L lanes
+// A tile is kStreamWaves waves x rpw rows x one column block.  Each wave
+// walks rpw consecutive rows; a row of the block is covered by L lanes
 // (L = 64 for wide blocks; narrow blocks put 64/L rows in one load), each
 // lane owning V consecutive columns.  Column sums accumulate in the lane's
 // registers while it walks down the rows; row sums are reduced across the
@@ -511,7 +511,7 @@ __global__ __launch_bounds__(kThreads) void ikfad_kernel(
 
 // ------------------------------------------------------------- probes
 
-// Each workgroup streams 4 KB per operand: four 16-byte non-temporal
+// Each workgroup streams 16 KB per operand: four 16-byte non-temporal
 // accesses per thread, all loads issued before any store.
 constexpr int kProbeUnroll = 4;
 
