@@ -350,6 +350,20 @@ def time_probe_write(nbytes, reps=50):
     return nbytes / (ms * 1e-3) / 1e9
 
 
+def measure_probes(n):
+    """The chip's ceilings for the step's access mixes over n elements:
+    the 3-read/2-write stream of five fp32 buffers, the step's own mix
+    without arithmetic (fp32 and bf16, contiguous and in the streaming
+    kernel's tiles), and read-only and write-only streams of 4 n bytes.
+    GB/s on each probe's own bytes."""
+    probes = {"stream_3r2w": time_probe(n)}
+    probes.update({f"mix_{dt}_{nm}": time_probe_mix(n, dt, sh)
+                   for dt in ("fp32", "bf16") for sh, nm in ((0, "contig"), (1, "tiles"))})
+    probes["read_only"] = time_probe_read(4 * n)
+    probes["write_only"] = time_probe_write(4 * n)
+    return probes
+
+
 def time_probe_read(nbytes, reps=50):
     """Read-only stream of nbytes.  GB/s."""
     import torch
@@ -517,16 +531,14 @@ def main():
             "hbm_gbps_step": rb["info"]["min_bytes_per_step"] / (rb["ms_per_step"] * 1e-3) / 1e9,
             "stream_ms": rb["stream_ms"],
             "stream_gbps": rb["info"]["stream_min_bytes"] / (rb["stream_ms"] * 1e-3) / 1e9}
-        var["probe_3r2w_gbps"] = time_probe(N)
-        var["stream_kernel_vs_probe"] = achieved / var["probe_3r2w_gbps"]
         # The chip's ceiling for each access mix, measured in the same run:
-        # the step's own mix without arithmetic (contiguous and in the
-        # streaming kernel's tiles) and a read-only stream of the gradient's
-        # fp32 bytes (what Adafactor-m's read passes move).
-        probes = {f"mix_{dt}_{nm}": time_probe_mix(N, dt, sh)
-                  for dt in ("fp32", "bf16") for sh, nm in ((0, "contig"), (1, "tiles"))}
-        probes["read_only"] = time_probe_read(4 * N)
-        probes["write_only"] = time_probe_write(4 * N)
+        # the plain 3-read/2-write stream, the step's own mix without
+        # arithmetic (contiguous and in the streaming kernel's tiles), and
+        # read-only (what Adafactor-m's read passes move) and write-only
+        # streams of the gradient's fp32 bytes.
+        probes = measure_probes(N)
+        var["probe_3r2w_gbps"] = probes.pop("stream_3r2w")
+        var["stream_kernel_vs_probe"] = achieved / var["probe_3r2w_gbps"]
         var["probes_gbps"] = probes
         ceil = {dt: max(probes[f"mix_{dt}_contig"], probes[f"mix_{dt}_tiles"],
                         *( [var["probe_3r2w_gbps"]] if dt == "fp32" else []))
